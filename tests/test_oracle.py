@@ -1,0 +1,262 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+Each test names what it pins. None of them re-types the oracle's formulas:
+they use scalar brute force, an independent masked formulation with autograd,
+finite differences, closed forms, invariants, special cases that reduce to
+torch's causal attention, and Lemma 1.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import causal_attention, grouped_oracle, key_gradients, query_rows
+from paper_2506_05433_amd.inputs import make_problem
+from tests._refs import brute_forward, packed_masked
+
+TENSORS = ("q_pre", "k_pre", "v_pre", "q_suf", "k_suf", "v_suf", "do_pre", "do_suf")
+
+
+def small(prefix, groups, suffix, h_q=2, h_kv=1, d=4, seed=0, scale=0.7):
+    prob = make_problem("tiny", seed=seed, lengths=(prefix, groups, suffix), h_q=h_q, h_kv=h_kv, head_dim=d,
+                        dtype="fp32", scale=scale)
+    t = {k: prob.as_float(k) for k in TENSORS}
+    return prob, t
+
+
+def run(prob, t, **kw):
+    return grouped_oracle(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, **kw)
+
+
+CASES = [
+    ((5,), (3,), (3, 1, 2)),
+    ((3, 4), (2, 1), (2, 3, 1)),
+    ((0,), (2,), (3, 2)),
+    ((4,), (0,), ()),
+    ((2, 3), (1, 2), (0, 2, 3)),
+]
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_forward_matches_scalar_brute_force(case):
+    """Pins Eq. (3) on every [P; R_i] (mask extents, softmax, ln-LSE, GQA map)."""
+    prob, t = small(*case)
+    ref = brute_forward(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale)
+    got = run(prob, t, grads=False, chunk=2)
+    for k in ("o_pre", "o_suf", "lse_pre", "lse_suf"):
+        np.testing.assert_allclose(got[k], ref[k], rtol=0, atol=1e-12, err_msg=k)
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_matches_packed_masked_autograd(case, torch_cpu):
+    """Lemma 1: the Eq. (2)/(4) grouped computation (autograd gradients) equals the repeated oracle."""
+    prob, t = small(*case, h_q=4, h_kv=2, d=8)
+    ref = packed_masked(torch_cpu, prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale)
+    got = run(prob, t, chunk=3)
+    for k in ("o_pre", "o_suf", "dq_pre", "dk_pre", "dv_pre", "dq_suf", "dk_suf", "dv_suf"):
+        np.testing.assert_allclose(got[k], ref[k], rtol=0, atol=1e-12, err_msg=k)
+
+
+def test_finite_differences():
+    """The backward is the vector-Jacobian product of L = sum(dO * O) (central differences, fp64)."""
+    prob, t = small((3,), (2,), (2, 3), h_q=2, h_kv=1, d=3, seed=3)
+    got = run(prob, t, chunk=2)
+
+    def loss(tt):
+        r = run(prob, tt, grads=False, chunk=2)
+        return float((r["o_pre"] * tt["do_pre"]).sum() + (r["o_suf"] * tt["do_suf"]).sum())
+
+    eps = 1e-6
+    for name in ("q_pre", "k_pre", "v_pre", "q_suf", "k_suf", "v_suf"):
+        fd = np.zeros_like(t[name])
+        for idx in np.ndindex(*t[name].shape):
+            tp = dict(t); tp[name] = t[name].copy(); tp[name][idx] += eps
+            tm = dict(t); tm[name] = t[name].copy(); tm[name][idx] -= eps
+            fd[idx] = (loss(tp) - loss(tm)) / (2 * eps)
+        np.testing.assert_allclose(got["d" + name], fd, rtol=1e-6, atol=1e-8, err_msg=name)
+
+
+def test_zero_queries_give_uniform_attention():
+    """Q = 0: every allowed key weighs the same, so LSE_t = ln(#keys) and O_t = mean of the allowed V rows.
+
+    Prefix row t sees t+1 keys, response row j sees P+j+1 (Eq. (1), causal).
+    """
+    prob, t = small((5, 2), (2, 1), (3, 4, 2), h_q=2, h_kv=2, d=3)
+    t["q_pre"][:] = 0
+    t["q_suf"][:] = 0
+    got = run(prob, t, grads=False)
+    cu_p, cu_s = prob.cu_prefix, prob.cu_suffix
+    m = 0
+    for g in range(2):
+        p0, p1 = cu_p[g], cu_p[g + 1]
+        P = p1 - p0
+        for j in range(P):
+            np.testing.assert_allclose(got["lse_pre"][:, p0 + j], math.log(j + 1), atol=1e-14)
+            np.testing.assert_allclose(got["o_pre"][p0 + j], t["v_pre"][p0:p0 + j + 1].mean(0), atol=1e-14)
+        for _ in range(prob.group_sizes[g]):
+            s0, s1 = cu_s[m], cu_s[m + 1]
+            for j in range(s1 - s0):
+                np.testing.assert_allclose(got["lse_suf"][:, s0 + j], math.log(P + j + 1), atol=1e-14)
+                allv = np.concatenate([t["v_pre"][p0:p1], t["v_suf"][s0:s0 + j + 1]], 0)
+                np.testing.assert_allclose(got["o_suf"][s0 + j], allv.mean(0), atol=1e-14)
+            m += 1
+
+
+def test_constant_values_kill_q_and_k_gradients():
+    """All V rows equal c: O = c everywhere and dQ = dK = 0 (softmax rows sum to one)."""
+    prob, t = small((4,), (3,), (2, 3, 1), h_q=2, h_kv=1, d=5)
+    c = np.array([0.3, -1.2, 2.0, 0.0, 0.7])
+    t["v_pre"][:] = c
+    t["v_suf"][:] = c
+    got = run(prob, t)
+    for k in ("o_pre", "o_suf"):
+        np.testing.assert_allclose(got[k], np.broadcast_to(c, got[k].shape), atol=1e-14)
+    for k in ("dq_pre", "dq_suf", "dk_pre", "dk_suf"):
+        assert np.abs(got[k]).max() < 1e-13, k
+
+
+def test_one_hot_diagonal_is_included():
+    """Orthogonal one-hot Q = K with a large scale: each row attends (almost) only to itself."""
+    prob, t = small((3,), (2,), (2, 3), h_q=1, h_kv=1, d=8, scale=60.0)
+    e = np.eye(8)
+    t["q_pre"][:, 0] = t["k_pre"][:, 0] = e[:3]
+    t["q_suf"][:2, 0] = t["k_suf"][:2, 0] = e[3:5]
+    t["q_suf"][2:, 0] = t["k_suf"][2:, 0] = e[5:8]
+    got = run(prob, t, grads=False)
+    np.testing.assert_allclose(got["o_pre"], t["v_pre"], atol=1e-20 + 1e-12)
+    np.testing.assert_allclose(got["o_suf"], t["v_suf"], atol=1e-12)
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_gradient_identities(case):
+    """Per (group, kv head): sum over keys of dK is 0; sum over keys of dV equals sum over queries of dO."""
+    prob, t = small(*case, h_q=4, h_kv=2, d=6)
+    got = run(prob, t)
+    cu_p, cu_s = prob.cu_prefix, prob.cu_suffix
+    m = 0
+    for g in range(len(prob.prefix_lens)):
+        p0, p1 = cu_p[g], cu_p[g + 1]
+        gs = prob.group_sizes[g]
+        s0, s1 = cu_s[m], cu_s[m + gs]
+        m += gs
+        for kv in range(2):
+            heads = [2 * kv, 2 * kv + 1]
+            dk = got["dk_pre"][p0:p1, kv].sum(0) + got["dk_suf"][s0:s1, kv].sum(0)
+            assert np.abs(dk).max() < 1e-12
+            dv = got["dv_pre"][p0:p1, kv].sum(0) + got["dv_suf"][s0:s1, kv].sum(0)
+            do = t["do_pre"][p0:p1][:, heads].sum((0, 1)) + t["do_suf"][s0:s1][:, heads].sum((0, 1))
+            np.testing.assert_allclose(dv, do, atol=1e-12)
+
+
+def test_single_member_is_causal_attention(torch_cpu):
+    """G = 1 reduces to ordinary causal attention over [P; R] (torch fp64 SDPA and autograd)."""
+    torch = torch_cpu
+    prob, t = small((6,), (1,), (5,), h_q=4, h_kv=2, d=8, seed=5)
+    got = run(prob, t, chunk=4)
+    cat = {n: np.concatenate([t[n + "_pre"], t[n + "_suf"]], 0) for n in ("q", "k", "v", "do")}
+    q = torch.tensor(cat["q"].transpose(1, 0, 2), requires_grad=True)
+    k = torch.tensor(np.repeat(cat["k"], 2, axis=1).transpose(1, 0, 2), requires_grad=True)
+    v = torch.tensor(np.repeat(cat["v"], 2, axis=1).transpose(1, 0, 2), requires_grad=True)
+    o = torch.nn.functional.scaled_dot_product_attention(q, k, v, is_causal=True, scale=prob.scale)
+    (o * torch.tensor(cat["do"].transpose(1, 0, 2))).sum().backward()
+    o = o.detach().numpy().transpose(1, 0, 2)
+    np.testing.assert_allclose(np.concatenate([got["o_pre"], got["o_suf"]]), o, atol=1e-12)
+    dq = q.grad.numpy().transpose(1, 0, 2)
+    dk = k.grad.numpy().transpose(1, 0, 2).reshape(11, 2, 2, 8).sum(2)
+    dv = v.grad.numpy().transpose(1, 0, 2).reshape(11, 2, 2, 8).sum(2)
+    np.testing.assert_allclose(np.concatenate([got["dq_pre"], got["dq_suf"]]), dq, atol=1e-12)
+    np.testing.assert_allclose(np.concatenate([got["dk_pre"], got["dk_suf"]]), dk, atol=1e-12)
+    np.testing.assert_allclose(np.concatenate([got["dv_pre"], got["dv_suf"]]), dv, atol=1e-12)
+
+
+def test_empty_prefix_is_independent_causal_attention(torch_cpu):
+    """P = 0: every response is an independent causal sequence."""
+    torch = torch_cpu
+    prob, t = small((0,), (3,), (4, 1, 3), h_q=2, h_kv=2, d=5)
+    got = run(prob, t)
+    cu = prob.cu_suffix
+    for m in range(3):
+        s0, s1 = cu[m], cu[m + 1]
+        q = torch.tensor(t["q_suf"][s0:s1].transpose(1, 0, 2), requires_grad=True)
+        k = torch.tensor(t["k_suf"][s0:s1].transpose(1, 0, 2), requires_grad=True)
+        v = torch.tensor(t["v_suf"][s0:s1].transpose(1, 0, 2), requires_grad=True)
+        o = torch.nn.functional.scaled_dot_product_attention(q, k, v, is_causal=True, scale=prob.scale)
+        (o * torch.tensor(t["do_suf"][s0:s1].transpose(1, 0, 2))).sum().backward()
+        np.testing.assert_allclose(got["o_suf"][s0:s1], o.detach().numpy().transpose(1, 0, 2), atol=1e-12)
+        np.testing.assert_allclose(got["dk_suf"][s0:s1], k.grad.numpy().transpose(1, 0, 2), atol=1e-12)
+        np.testing.assert_allclose(got["dq_suf"][s0:s1], q.grad.numpy().transpose(1, 0, 2), atol=1e-12)
+
+
+def test_zero_prefix_upstream_gradient_gives_zero_prefix_dq():
+    """dO_pre = 0 (the final-layer situation of the proof: the loss only reads responses) => dQ_pre = 0."""
+    prob, t = small((4,), (3,), (2, 2, 3), h_q=2, h_kv=1, d=4)
+    t["do_pre"][:] = 0
+    got = run(prob, t)
+    assert np.abs(got["dq_pre"]).max() == 0.0
+    assert np.abs(got["dk_pre"]).max() > 0
+
+
+def test_prefix_rows_agree_bitwise_across_members():
+    """Lemma 1, forward: every member's copy of the prefix gives identical outputs."""
+    prob, t = small((7,), (4,), (2, 5, 1, 3), h_q=2, h_kv=1, d=6)
+    got = run(prob, t, chunk=3)
+    assert got["prefix_member_spread"] == 0.0
+
+
+def test_backward_is_linear_in_upstream_gradient():
+    """VJP linearity: grad(a*dO1 + b*dO2) = a*grad(dO1) + b*grad(dO2); the prefix split over copies is free."""
+    prob, t = small((4, 3), (2, 2), (3, 1, 2, 2), h_q=2, h_kv=1, d=4)
+    _, t2 = small((4, 3), (2, 2), (3, 1, 2, 2), h_q=2, h_kv=1, d=4, seed=9)
+    g1 = run(prob, t)
+    tb = dict(t); tb["do_pre"] = t2["do_pre"]; tb["do_suf"] = t2["do_suf"]
+    g2 = run(prob, tb)
+    tc = dict(t); tc["do_pre"] = 2 * t["do_pre"] - 3 * t2["do_pre"]; tc["do_suf"] = 2 * t["do_suf"] - 3 * t2["do_suf"]
+    g3 = run(prob, tc)
+    for k in ("dq_pre", "dk_pre", "dv_pre", "dq_suf", "dk_suf", "dv_suf"):
+        np.testing.assert_allclose(g3[k], 2 * g1[k] - 3 * g2[k], atol=1e-12, err_msg=k)
+
+
+def test_member_permutation():
+    """Permuting the members of a group permutes the response results; prefix results agree to rounding."""
+    prob, t = small((4,), (3,), (2, 3, 1), h_q=2, h_kv=1, d=4)
+    got = run(prob, t)
+    perm = [2, 0, 1]
+    cu = prob.cu_suffix
+    rows = np.concatenate([np.arange(cu[m], cu[m + 1]) for m in perm])
+    tp = dict(t)
+    for n in ("q_suf", "k_suf", "v_suf", "do_suf"):
+        tp[n] = t[n][rows]
+    prob_p, _ = small((4,), (3,), tuple(prob.suffix_lens[perm]), h_q=2, h_kv=1, d=4)
+    got_p = grouped_oracle(prob_p.prefix_lens, prob_p.group_sizes, prob_p.suffix_lens, tp, prob.scale)
+    for n in ("o_suf", "dq_suf", "dk_suf", "dv_suf"):
+        np.testing.assert_allclose(got_p[n], got[n][rows], atol=1e-14)
+    for n in ("o_pre", "dq_pre", "dk_pre", "dv_pre"):
+        np.testing.assert_allclose(got_p[n], got[n], atol=1e-13)
+
+
+def test_query_rows_and_key_gradients_match_full_oracle():
+    """The sampled-row and sampled-key oracles agree with the full oracle (used at full workload sizes)."""
+    prob, t = small((6, 5), (3, 2), (4, 2, 5, 3, 1), h_q=4, h_kv=2, d=8)
+    full = run(prob, t, chunk=4)
+    heads = [0, 3]
+    for side, rows in (("pre", [0, 5, 6, 10]), ("suf", [0, 3, 6, 10, 14])):
+        r = query_rows(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, side, rows, heads)
+        np.testing.assert_allclose(r["o"], full["o_" + side][rows][:, heads], atol=1e-12)
+        np.testing.assert_allclose(r["lse"], full["lse_" + side][heads][:, rows], atol=1e-12)
+        np.testing.assert_allclose(r["dq"], full["dq_" + side][rows][:, heads], atol=1e-12)
+    for g, side, keys in ((0, "pre", [0, 2, 5]), (1, "pre", [6, 10]), (0, "suf", [0, 5, 10]), (1, "suf", [11, 14])):
+        for kv in range(2):
+            r = key_gradients(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, g, kv, side,
+                              keys, chunk=3)
+            np.testing.assert_allclose(r["dk"], full["dk_" + side][keys, kv], atol=1e-12)
+            np.testing.assert_allclose(r["dv"], full["dv_" + side][keys, kv], atol=1e-12)
+
+
+def test_causal_attention_chunking_is_exact():
+    """Row chunking only bounds memory: any chunk size gives the same numbers."""
+    rng = np.random.default_rng(1)
+    q, k, v, do = (rng.standard_normal((9, 2, 3)) for _ in range(4))
+    a = causal_attention(q, k[:, :1], v[:, :1], 0.5, do=do, split=4, chunk=2)
+    b = causal_attention(q, k[:, :1], v[:, :1], 0.5, do=do, split=None, chunk=100)
+    for key in a:
+        np.testing.assert_allclose(a[key], b[key], atol=1e-13)
