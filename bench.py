@@ -1,0 +1,195 @@
+"""Benchmark: grouped (shared-prefix) attention forward+backward on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--no-repeated]
+
+A step is one forward and one backward call over the whole workload (inputs
+resident in HBM). Prints ONE JSON line. ``value`` is useful TFLOP/s:
+4*d*H_q*pairs (forward) + 10*d*H_q*pairs (backward) per step, where pairs is
+the exact number of (query, key) pairs the grouped problem allows; masked
+work, ragged tiles and the repeated-prefix pairs the method avoids are not
+counted. The same kernels are also timed on the repeated-prefix layout
+(every member with its own copy of the prefix) for the speedup.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "grouped attn fwd+bwd TFLOP/s (useful) & % MFMA peak; speedup vs repeated-prefix"
+PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
+
+
+def pair_count(prefix_lens, group_sizes, suffix_lens):
+    """Allowed (query, key) pairs of the grouped problem: prefix row t sees t+1 keys, response row j sees P+j+1."""
+    total = 0
+    m = 0
+    for p, g in zip(prefix_lens, group_sizes):
+        p = int(p)
+        total += p * (p + 1) // 2
+        for s in suffix_lens[m:m + int(g)]:
+            s = int(s)
+            total += s * p + s * (s + 1) // 2
+        m += int(g)
+    return total
+
+
+def repeated_pair_count(prefix_lens, group_sizes, suffix_lens):
+    total, m = 0, 0
+    for p, g in zip(prefix_lens, group_sizes):
+        for s in suffix_lens[m:m + int(g)]:
+            n = int(p) + int(s)
+            total += n * (n + 1) // 2
+        m += int(g)
+    return total
+
+
+def time_steps(binding, torch, dev, bufs, steps, warmup):
+    def step():
+        binding.fwd(dev["q_pre"], dev["k_pre"], dev["v_pre"], dev["q_suf"], dev["k_suf"], dev["v_suf"],
+                    dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], dev["scale"], out=bufs["fwd"],
+                    workspace=bufs["ws_f"])
+        o_pre, o_suf, lse_pre, lse_suf = bufs["fwd"]
+        binding.bwd(dev["q_pre"], dev["k_pre"], dev["v_pre"], dev["q_suf"], dev["k_suf"], dev["v_suf"],
+                    o_pre, o_suf, lse_pre, lse_suf, dev["do_pre"], dev["do_suf"],
+                    dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], dev["scale"], out=bufs["bwd"],
+                    workspace=bufs["ws_b"])
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    binding.timing_start()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    binding.timing_stop()
+    ms = e0.elapsed_time(e1) / steps
+    kern = {}
+    for k in ("plan", "fwd", "bwd_dot", "dkdv", "dq"):
+        n, tot = binding.timing_get(k)
+        kern[k] = {"launches": n, "avg_ms": (tot / n) if n else None}
+    return ms, kern
+
+
+def alloc(binding, torch, dev, prob):
+    bufs = {
+        "fwd": (torch.empty_like(dev["q_pre"]), torch.empty_like(dev["q_suf"]),
+                torch.empty((prob.h_q, prob.total_prefix), device="cuda", dtype=torch.float32),
+                torch.empty((prob.h_q, prob.total_suffix), device="cuda", dtype=torch.float32)),
+        "bwd": tuple(torch.empty_like(dev[k]) for k in ("q_pre", "k_pre", "v_pre", "q_suf", "k_suf", "v_suf")),
+    }
+    args = (len(prob.prefix_lens), len(prob.suffix_lens), prob.total_prefix, prob.total_suffix, prob.h_q)
+    bufs["ws_f"] = torch.empty(binding.workspace_bytes("fwd", *args), device="cuda", dtype=torch.uint8)
+    bufs["ws_b"] = torch.empty(binding.workspace_bytes("bwd", *args), device="cuda", dtype=torch.uint8)
+    return bufs
+
+
+def cpu_baseline(prob, useful_per_pair_head, budget_s):
+    """The oracle (fp64 numpy, as it stands) on a bounded sample: all rows, a few query heads."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import grouped_oracle
+    n_heads = 1
+    t = {k: prob.as_float(k, np.float64) for k in prob.tensors}
+    pairs_rep = repeated_pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
+    pairs = pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
+    t0 = time.perf_counter()
+    grouped_oracle(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, grads=True,
+                   heads=list(range(n_heads)), check_members=False)
+    dt = time.perf_counter() - t0
+    # grow the sample toward the budget if the first head was quick
+    if dt < budget_s / 3 and prob.h_q > 1:
+        n_heads = max(1, min(prob.h_q, int(budget_s / max(dt, 1e-3) * 0.5)))
+        t0 = time.perf_counter()
+        grouped_oracle(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, grads=True,
+                       heads=list(range(n_heads)), check_members=False)
+        dt = time.perf_counter() - t0
+    useful = useful_per_pair_head * pairs * n_heads
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": useful / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n_heads} of {prob.h_q} query heads, all rows and members, fp64 numpy, repeated-prefix "
+                      f"({pairs_rep} repeated pairs per head), fwd+bwd; {dt:.1f} s",
+            "seconds": dt, "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="single_group")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-repeated", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2506_05433_amd import binding
+    from paper_2506_05433_amd.inputs import WORKLOADS, make_problem, repeated_layout
+
+    wl = WORKLOADS[args.workload]
+    prob = make_problem(wl, seed=0)
+    d, hq = prob.head_dim, prob.h_q
+    pairs = pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
+    rep_pairs = repeated_pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
+    fwd_flops = 4.0 * d * hq * pairs
+    bwd_flops = 10.0 * d * hq * pairs
+    dev = binding.to_device(prob, "cuda")
+    bufs = alloc(binding, torch, dev, prob)
+    print(f"[bench] {wl.name}: pairs={pairs} tokens={prob.total_prefix + prob.total_suffix}", file=sys.stderr,
+          flush=True)
+    ms, kern = time_steps(binding, torch, dev, bufs, args.steps, args.warmup)
+    value = (fwd_flops + bwd_flops) / (ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[prob.dtype]
+    algo = {"fwd": fwd_flops, "dkdv": 8.0 * d * hq * pairs, "dq": 6.0 * d * hq * pairs}
+    dom = max(("fwd", "dkdv", "dq"), key=lambda k: (kern[k]["avg_ms"] or 0.0))
+    achieved = algo[dom] / (kern[dom]["avg_ms"] * 1e-3) / 1e12
+    fwd_ms = kern["fwd"]["avg_ms"]
+    bwd_ms = sum(kern[k]["avg_ms"] or 0.0 for k in ("bwd_dot", "dkdv", "dq"))
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": prob.dtype, "data": "synthetic (seeded normal inputs, lengths drawn per workload)",
+        "config": {"workload": wl.name, "desc": wl.note, "n_groups": int(len(prob.prefix_lens)),
+                   "total_prefix": prob.total_prefix, "total_suffix": prob.total_suffix, "h_q": hq,
+                   "h_kv": prob.h_kv, "head_dim": d, "pairs": pairs, "parallelism": "single GPU"},
+        "pct_of_peak": round(100.0 * value / peak, 2),
+        "fwd_tflops": round(fwd_flops / (fwd_ms * 1e-3) / 1e12, 2) if fwd_ms else None,
+        "bwd_tflops": round(bwd_flops / (bwd_ms * 1e-3) / 1e12, 2) if bwd_ms else None,
+        "kernels_ms": {k: (round(v["avg_ms"], 4) if v["avg_ms"] else None) for k, v in kern.items()},
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None},
+    }
+    if not args.no_repeated:
+        rep = repeated_layout(prob)
+        del dev, bufs
+        torch.cuda.empty_cache()
+        rdev = binding.to_device(rep, "cuda")
+        rbufs = alloc(binding, torch, rdev, rep)
+        rms, _ = time_steps(binding, torch, rdev, rbufs, args.steps, args.warmup)
+        G = prob.group_sizes
+        P = prob.prefix_lens
+        sum_s = prob.suffix_lens.sum()
+        target = 0.8 * float((G * P).sum() + sum_s) / float(P.sum() + sum_s)
+        out.update({"repeated_ms_per_step": round(rms, 4), "speedup_vs_repeated": round(rms / ms, 3),
+                    "speedup_target": round(target, 3), "speedup_ceiling_pairs": round(rep_pairs / pairs, 3)})
+        del rdev, rbufs
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(prob, 14.0 * d, args.cpu_budget)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,143 @@
+/*
+ * pg_attn.h -- grouped (shared-prefix) causal attention for AMD MI355X (gfx950).
+ *
+ * The operation is the Grouped Attention of Prefix Grouper (Section 2.1,
+ * Eq. (4) and Algorithm 1): for every group, the shared prefix runs causal
+ * self-attention once, and each of the group's G responses ("suffixes") runs
+ * concat-attention whose queries see the whole prefix plus their own
+ * response up to themselves. By Lemma 1 (Section 2.2) the outputs equal
+ * standard causal attention over every [prefix; response_i] sequence
+ * (Repeated-Prefix Forward, Eq. (1) and (3)), and the gradient of the shared
+ * prefix is the sum of the gradients its G copies would receive there.
+ *
+ * Layout (all tensors contiguous, row-major, token-major "packed varlen"):
+ *   q_pre, o_pre, do_pre, dq_pre : [total_prefix, h_q,  head_dim]
+ *   k_pre, v_pre, dk_pre, dv_pre : [total_prefix, h_kv, head_dim]
+ *   q_suf, o_suf, do_suf, dq_suf : [total_suffix, h_q,  head_dim]
+ *   k_suf, v_suf, dk_suf, dv_suf : [total_suffix, h_kv, head_dim]
+ *   lse_pre : float [h_q, total_prefix],  lse_suf : float [h_q, total_suffix]
+ * Element type: bfloat16 (PG_BF16) or float (PG_FP32) for every tensor
+ * except the log-sum-exp, which is always float (natural log).
+ *
+ * Grouping (device int32 arrays):
+ *   cu_prefix_lens [n_groups+1]  : group g owns prefix rows
+ *                                  [cu_prefix_lens[g], cu_prefix_lens[g+1]);
+ *                                  [0] = 0, nondecreasing, [n_groups] = total_prefix.
+ *   cu_suffix_lens [n_suffixes+1]: member m owns suffix rows
+ *                                  [cu_suffix_lens[m], cu_suffix_lens[m+1]);
+ *                                  [0] = 0, nondecreasing, [n_suffixes] = total_suffix.
+ *   group_sizes    [n_groups]    : members per group, >= 0, summing to n_suffixes;
+ *                                  members of group g follow those of group g-1.
+ * Empty prefixes, empty responses and groups without members are legal.
+ * GQA: query head h reads key/value head h / (h_q / h_kv); h_q % h_kv == 0.
+ * head_dim must be 64 or 128. softmax_scale multiplies q.k before the softmax
+ * (q and k arrive already rotary-encoded, as Algorithm 1 requires).
+ *
+ * Ownership and execution: every pointer except those of the size queries is
+ * DEVICE memory owned by the caller. The library allocates nothing and keeps
+ * no pointer after a call returns. Calls are asynchronous and ordered on the
+ * given HIP stream (a hipStream_t passed as void*, NULL = the null stream).
+ * Outputs are overwritten, never accumulated. Results are bitwise
+ * deterministic for identical inputs (no floating-point atomics).
+ *
+ * Errors: each call returns a pg_status. Host-side argument checks run before
+ * anything is launched, and on error no output is touched. The consistency of
+ * the device grouping arrays is checked on the device: if they are
+ * inconsistent no attention work is done (outputs are left as they were) and,
+ * only when the environment variable PG_DEBUG_VALIDATE=1 is set (which makes
+ * the call synchronise), PG_EINVAL is returned. HIP failures return PG_EHIP.
+ * pg_last_error() gives a message for the calling thread's last failure.
+ */
+#ifndef PG_ATTN_H
+#define PG_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { PG_BF16 = 0, PG_FP32 = 1 } pg_dtype;
+
+typedef enum {
+  PG_OK = 0,
+  PG_EINVAL = 1,       /* bad argument (sizes, null pointers, scale, grouping arrays) */
+  PG_EUNSUPPORTED = 2, /* valid but unsupported (head_dim, dtype)                      */
+  PG_EWORKSPACE = 3,   /* workspace missing or smaller than the size query returns     */
+  PG_EHIP = 4          /* HIP runtime failure (no device, launch error, ...)           */
+} pg_status;
+
+/* Workspace bytes pg_attn_fwd needs for these sizes (host call, no GPU use). */
+size_t pg_attn_fwd_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q);
+
+/* Workspace bytes pg_attn_bwd needs for these sizes (host call, no GPU use). */
+size_t pg_attn_bwd_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q);
+
+/*
+ * Forward pass: Eq. (4). Writes o_pre, o_suf and the natural-log
+ * log-sum-exp of every query row, lse = ln sum_s exp(softmax_scale * q.k_s)
+ * over the keys the row sees (prefix row t of a group: prefix keys 0..t;
+ * response row j of member i: the whole prefix and response keys 0..j of
+ * member i). The log-sum-exp is what pg_attn_bwd consumes.
+ */
+int pg_attn_fwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                int h_q, int h_kv, int head_dim, float softmax_scale,
+                const void* q_pre, const void* k_pre, const void* v_pre,
+                const void* q_suf, const void* k_suf, const void* v_suf,
+                void* o_pre, void* o_suf, float* lse_pre, float* lse_suf,
+                void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Backward pass: the vector-Jacobian product of the forward with upstream
+ * gradients do_pre, do_suf (Lemma 1 and its proof, Appendix A.1). dq/dk/dv of
+ * the suffix rows are those of each member's own rows; dq_pre, dk_pre, dv_pre
+ * are the full gradients of the shared prefix, i.e. summed over all G members
+ * (and, for dk/dv, over the query heads sharing a key/value head), reduced in
+ * a fixed order. o_* and lse_* must be the forward's outputs for the same
+ * inputs.
+ */
+int pg_attn_bwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                int h_q, int h_kv, int head_dim, float softmax_scale,
+                const void* q_pre, const void* k_pre, const void* v_pre,
+                const void* q_suf, const void* k_suf, const void* v_suf,
+                const void* o_pre, const void* o_suf, const float* lse_pre, const float* lse_suf,
+                const void* do_pre, const void* do_suf,
+                void* dq_pre, void* dk_pre, void* dv_pre,
+                void* dq_suf, void* dk_suf, void* dv_suf,
+                void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Kernel timing for benchmarks. Between pg_timing_start() and pg_timing_stop()
+ * every call brackets each of its kernel launches with a pair of HIP events
+ * recorded on the call's stream (at most 16384 launches are recorded per start;
+ * later ones are not). pg_timing_get() waits for the recorded events and
+ * returns, for one kernel kind, how many launches were recorded and their
+ * summed duration in milliseconds. pg_timing_start() discards earlier records.
+ * Not meant to be used while other threads issue calls.
+ */
+typedef enum {
+  PG_K_PLAN = 0,     /* the planner kernels of one call, as one interval      */
+  PG_K_FWD = 1,      /* forward attention kernel                              */
+  PG_K_BWD_DOT = 2,  /* backward: rowsum(dO * O)                              */
+  PG_K_DKDV = 3,     /* backward: dK, dV (key-stationary, G-way prefix sum)   */
+  PG_K_DQ = 4        /* backward: dQ (query-stationary)                       */
+} pg_kernel;
+
+int pg_timing_start(void);
+int pg_timing_stop(void);
+int pg_timing_get(int kernel, int* launches, double* total_ms);
+
+/* Static description of a status code. */
+const char* pg_status_string(int status);
+
+/* Message for the calling thread's most recent failing call ("" if none). */
+const char* pg_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PG_ATTN_H */

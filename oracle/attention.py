@@ -256,16 +256,21 @@ def query_rows(prefix_lens, group_sizes, suffix_lens, t, scale, side, rows, head
 
 
 def key_gradients(prefix_lens, group_sizes, suffix_lens, t, scale, group, kv_head, side, keys,
-                  dtype=np.float64, chunk=1024):
+                  dtype=np.float64, chunk=1024, heads=None):
     """dK and dV of selected keys of one group and one key/value head.
 
     The gradient of key s is the sum over every query that sees s (Eq. (3)
     backward): dk_s = scale * sum_t dz_ts q_t and dv_s = sum_t a_ts do_t, over
-    the query heads that share ``kv_head``. For a prefix key the queries are
-    the prefix rows of every member copy (each with do_pre / G) and every
-    member's response rows; the copies are summed in member order (Lemma 1).
-    The softmax statistics of each query row come from that row's full key
-    set, computed exactly per row chunk.
+    the query heads that share ``kv_head`` (or only ``heads`` if given). The
+    queries of a prefix key are the group's prefix rows at or after it and
+    every response row of every member; the queries of a response key are the
+    rows of its own member at or after it.
+
+    Each distinct query row is evaluated once, from its full key set. In the
+    repeated computation a prefix row exists G times, every copy sees the same
+    keys and carries do_pre / G, so the G copies together contribute exactly
+    one evaluation with do_pre (the VJP is linear in dO; Lemma 1). This keeps
+    the cost at the grouped size, which makes full-size workloads checkable.
 
     ``side`` is "pre" or "suf" and ``keys`` are packed row indices on that
     side (suffix keys must belong to ``group``). Returns dk, dv [len(keys), d].
@@ -275,50 +280,52 @@ def key_gradients(prefix_lens, group_sizes, suffix_lens, t, scale, group, kv_hea
     g_members = _group_members(group_sizes)
     h_q, d = t["q_pre"].shape[1], t["q_pre"].shape[2]
     h_kv = t["k_pre"].shape[1]
-    heads = [h for h in range(h_q) if _kv_head(h, h_q, h_kv) == kv_head]
+    if heads is None:
+        heads = [h for h in range(h_q) if _kv_head(h, h_q, h_kv) == kv_head]
     p0, p1 = int(cu_p[group]), int(cu_p[group + 1])
     plen = p1 - p0
     m0, m1 = g_members[group]
-    members = list(range(m0, m1)) if m1 > m0 else [None]
-    share = 1.0 / (m1 - m0) if m1 > m0 else 1.0
     keys = [int(s) for s in keys]
     dk = np.zeros((len(keys), d), dtype)
     dv = np.zeros((len(keys), d), dtype)
-    for m in members:
-        s0, s1 = (int(cu_s[m]), int(cu_s[m + 1])) if m is not None else (0, 0)
-        # positions of the selected keys inside this member's sequence [P; R_m]
-        pos = []
-        for s in keys:
+    kp = np.asarray(t["k_pre"][p0:p1, kv_head, :], dtype)
+    vp = np.asarray(t["v_pre"][p0:p1, kv_head, :], dtype)
+
+    def accumulate(q, do, k, v, first_row, n_rows, cols):
+        # rows first_row .. first_row+n_rows-1 of a sequence whose key j is k[j]; row r sees keys 0..r
+        for r0 in range(first_row, first_row + n_rows, chunk):
+            r1 = min(first_row + n_rows, r0 + chunk)
+            z = scale * (q[r0 - first_row:r1 - first_row] @ k[:r1].T)
+            rows = np.arange(r0, r1)[:, None]
+            z = np.where(np.arange(r1)[None, :] <= rows, z, -np.inf)
+            mx = z.max(axis=1, keepdims=True)
+            a = np.exp(z - (mx + np.log(np.exp(z - mx).sum(axis=1, keepdims=True))))
+            dos = do[r0 - first_row:r1 - first_row]
+            da = dos @ v[:r1].T
+            dz = a * (da - (a * da).sum(axis=1, keepdims=True))
+            qs = q[r0 - first_row:r1 - first_row]
+            for j, c in cols:
+                if c < r1:
+                    dk[j] += scale * (dz[:, c] @ qs)
+                    dv[j] += a[:, c] @ dos
+
+    for h in heads:
+        if side == "pre":
+            cols = [(j, s - p0) for j, s in enumerate(keys)]
+            qp = np.asarray(t["q_pre"][p0:p1, h, :], dtype)
+            dop = np.asarray(t["do_pre"][p0:p1, h, :], dtype)
+            accumulate(qp, dop, kp, vp, 0, plen, cols)
+        for m in range(m0, m1):
+            s0, s1 = int(cu_s[m]), int(cu_s[m + 1])
             if side == "pre":
-                pos.append(s - p0)
+                cols = [(j, s - p0) for j, s in enumerate(keys)]
             else:
-                pos.append(plen + (s - s0) if s0 <= s < s1 else -1)
-        if all(p_ < 0 for p_ in pos):
-            continue
-        pos_arr = np.array(pos)
-        cat = lambda a, b: np.concatenate([t[a][p0:p1], t[b][s0:s1]], 0).astype(dtype)  # noqa: E731
-        k, v = cat("k_pre", "k_suf")[:, kv_head, :], cat("v_pre", "v_suf")[:, kv_head, :]
-        n = k.shape[0]
-        bounds = [0]
-        for edge in ([plen] if 0 < plen < n else []) + [n]:
-            while bounds[-1] < edge:
-                bounds.append(min(edge, bounds[-1] + chunk))
-        for h in heads:
-            q = cat("q_pre", "q_suf")[:, h, :]
-            do = np.concatenate([t["do_pre"][p0:p1, h, :].astype(dtype) * dtype(share),
-                                 t["do_suf"][s0:s1, h, :].astype(dtype)], 0)
-            for r0, r1 in zip(bounds[:-1], bounds[1:]):
-                z = scale * (q[r0:r1] @ k[:r1].T)
-                rows = np.arange(r0, r1)[:, None]
-                cols = np.arange(r1)[None, :]
-                z = np.where(cols <= rows, z, -np.inf)
-                mx = z.max(axis=1, keepdims=True)
-                lse = mx + np.log(np.exp(z - mx).sum(axis=1, keepdims=True))
-                a = np.exp(z - lse)
-                da = do[r0:r1] @ v[:r1].T
-                dz = a * (da - (a * da).sum(axis=1, keepdims=True))
-                for j, p_ in enumerate(pos_arr):
-                    if 0 <= p_ < r1:
-                        dk[j] += scale * (dz[:, p_] @ q[r0:r1])
-                        dv[j] += a[:, p_] @ do[r0:r1]
+                cols = [(j, plen + s - s0) for j, s in enumerate(keys) if s0 <= s < s1]
+            if not cols or s1 == s0:
+                continue
+            k = np.concatenate([kp, np.asarray(t["k_suf"][s0:s1, kv_head, :], dtype)], 0)
+            v = np.concatenate([vp, np.asarray(t["v_suf"][s0:s1, kv_head, :], dtype)], 0)
+            qs = np.asarray(t["q_suf"][s0:s1, h, :], dtype)
+            dos = np.asarray(t["do_suf"][s0:s1, h, :], dtype)
+            accumulate(qs, dos, k, v, plen, s1 - s0, cols)
     return {"dk": dk, "dv": dv}

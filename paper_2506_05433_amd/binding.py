@@ -1,0 +1,192 @@
+"""Thin ctypes binding of ``libpg_attn.so`` (argument marshalling only).
+
+Every step of the computation runs in the HIP library; this module only turns
+torch device tensors into pointers and sizes, allocates outputs and the
+workspace with torch, and passes the current HIP stream. It fails loudly when
+the library has not been built: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libpg_attn.so")
+
+PG_BF16, PG_FP32 = 0, 1
+STATUS = {0: "PG_OK", 1: "PG_EINVAL", 2: "PG_EUNSUPPORTED", 3: "PG_EWORKSPACE", 4: "PG_EHIP"}
+
+_lib = None
+
+# names and argument types of every function include/pg_attn.h declares
+_I, _Z, _F, _P = ctypes.c_int, ctypes.c_size_t, ctypes.c_float, ctypes.c_void_p
+SIGNATURES = {
+    "pg_attn_fwd_workspace_size": (_Z, [_I, _I, _I, _I, _I]),
+    "pg_attn_bwd_workspace_size": (_Z, [_I, _I, _I, _I, _I]),
+    "pg_attn_fwd": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 10 + [_P, _Z, _P]),
+    "pg_attn_bwd": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 18 + [_P, _Z, _P]),
+    "pg_timing_start": (_I, []),
+    "pg_timing_stop": (_I, []),
+    "pg_timing_get": (_I, [_I, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)]),
+    "pg_status_string": (ctypes.c_char_p, [_I]),
+    "pg_last_error": (ctypes.c_char_p, []),
+}
+
+
+class PgError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2506_05433_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+KERNELS = {"plan": 0, "fwd": 1, "bwd_dot": 2, "dkdv": 3, "dq": 4}
+
+
+def timing_start():
+    _check(lib().pg_timing_start())
+
+
+def timing_stop():
+    _check(lib().pg_timing_stop())
+
+
+def timing_get(kernel: str):
+    """(launches, total_ms) recorded for one kernel kind since timing_start()."""
+    n, ms = ctypes.c_int(0), ctypes.c_double(0.0)
+    _check(lib().pg_timing_get(KERNELS[kernel], ctypes.byref(n), ctypes.byref(ms)))
+    return n.value, ms.value
+
+
+def _check(status: int):
+    if status != 0:
+        raise PgError(status, lib().pg_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(torch, dt):
+    if dt == torch.bfloat16:
+        return PG_BF16
+    if dt == torch.float32:
+        return PG_FP32
+    raise TypeError(f"unsupported dtype {dt}")
+
+
+def _stream(torch, device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def workspace_bytes(kind: str, n_groups, n_suffixes, total_prefix, total_suffix, h_q) -> int:
+    fn = lib().pg_attn_fwd_workspace_size if kind == "fwd" else lib().pg_attn_bwd_workspace_size
+    return int(fn(n_groups, n_suffixes, total_prefix, total_suffix, h_q))
+
+
+def _shapes(q_pre, k_pre, q_suf, cu_prefix, cu_suffix, group_sizes):
+    n_groups = group_sizes.numel()
+    n_suffixes = cu_suffix.numel() - 1
+    if cu_prefix.numel() != n_groups + 1:
+        raise ValueError("cu_prefix_lens must have n_groups + 1 entries")
+    for t in (cu_prefix, cu_suffix, group_sizes):
+        if t.dtype.itemsize != 4 or t.dtype.is_floating_point or not t.is_contiguous():
+            raise TypeError("grouping arrays must be contiguous int32 device tensors")
+    return n_groups, n_suffixes, q_pre.shape[0], q_suf.shape[0], q_pre.shape[1], k_pre.shape[1], q_pre.shape[2]
+
+
+def fwd(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, cu_prefix, cu_suffix, group_sizes, scale,
+        out=None, workspace=None):
+    """Grouped attention forward. Returns (o_pre, o_suf, lse_pre, lse_suf)."""
+    import torch
+    ng, ns, tp, ts, hq, hkv, d = _shapes(q_pre, k_pre, q_suf, cu_prefix, cu_suffix, group_sizes)
+    dev = q_pre.device
+    if out is None:
+        out = (torch.empty_like(q_pre), torch.empty_like(q_suf),
+               torch.empty((hq, tp), device=dev, dtype=torch.float32),
+               torch.empty((hq, ts), device=dev, dtype=torch.float32))
+    need = workspace_bytes("fwd", ng, ns, tp, ts, hq)
+    if workspace is None:
+        workspace = torch.empty(need, device=dev, dtype=torch.uint8)
+    o_pre, o_suf, lse_pre, lse_suf = out
+    st = lib().pg_attn_fwd(
+        _dtype_code(torch, q_pre.dtype), ng, ns, tp, ts,
+        _ptr(cu_prefix), _ptr(cu_suffix), _ptr(group_sizes), hq, hkv, d, float(scale),
+        _ptr(q_pre), _ptr(k_pre), _ptr(v_pre), _ptr(q_suf), _ptr(k_suf), _ptr(v_suf),
+        _ptr(o_pre), _ptr(o_suf), _ptr(lse_pre), _ptr(lse_suf),
+        _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(torch, dev))
+    _check(st)
+    return o_pre, o_suf, lse_pre, lse_suf
+
+
+def bwd(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, o_pre, o_suf, lse_pre, lse_suf, do_pre, do_suf,
+        cu_prefix, cu_suffix, group_sizes, scale, out=None, workspace=None):
+    """Grouped attention backward. Returns (dq_pre, dk_pre, dv_pre, dq_suf, dk_suf, dv_suf)."""
+    import torch
+    ng, ns, tp, ts, hq, hkv, d = _shapes(q_pre, k_pre, q_suf, cu_prefix, cu_suffix, group_sizes)
+    dev = q_pre.device
+    if out is None:
+        out = (torch.empty_like(q_pre), torch.empty_like(k_pre), torch.empty_like(v_pre),
+               torch.empty_like(q_suf), torch.empty_like(k_suf), torch.empty_like(v_suf))
+    need = workspace_bytes("bwd", ng, ns, tp, ts, hq)
+    if workspace is None:
+        workspace = torch.empty(need, device=dev, dtype=torch.uint8)
+    st = lib().pg_attn_bwd(
+        _dtype_code(torch, q_pre.dtype), ng, ns, tp, ts,
+        _ptr(cu_prefix), _ptr(cu_suffix), _ptr(group_sizes), hq, hkv, d, float(scale),
+        _ptr(q_pre), _ptr(k_pre), _ptr(v_pre), _ptr(q_suf), _ptr(k_suf), _ptr(v_suf),
+        _ptr(o_pre), _ptr(o_suf), _ptr(lse_pre), _ptr(lse_suf), _ptr(do_pre), _ptr(do_suf),
+        *[_ptr(t) for t in out],
+        _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(torch, dev))
+    _check(st)
+    return out
+
+
+def to_device(prob, device="cuda"):
+    """Copy a seeded problem (``paper_2506_05433_amd.inputs.Problem``) to device tensors.
+
+    Returns a dict with the eight tensors (bfloat16 or float32), the int32
+    grouping arrays ``cu_prefix``, ``cu_suffix``, ``group_sizes`` and ``scale``.
+    """
+    import numpy as np
+    import torch
+    out = {}
+    for name, a in prob.tensors.items():
+        if a.dtype == np.uint16:
+            t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16)
+        else:
+            t = torch.from_numpy(np.ascontiguousarray(a))
+        out[name] = t.to(device)
+    out["cu_prefix"] = torch.from_numpy(prob.cu_prefix.astype(np.int32)).to(device)
+    out["cu_suffix"] = torch.from_numpy(prob.cu_suffix.astype(np.int32)).to(device)
+    out["group_sizes"] = torch.from_numpy(prob.group_sizes.astype(np.int32)).to(device)
+    out["scale"] = prob.scale
+    return out
+
+
+def run_fwd(dev):
+    """Forward on a ``to_device`` dict."""
+    return fwd(dev["q_pre"], dev["k_pre"], dev["v_pre"], dev["q_suf"], dev["k_suf"], dev["v_suf"],
+               dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], dev["scale"])
+
+
+def run_bwd(dev, fwd_out):
+    """Backward on a ``to_device`` dict and the forward's outputs."""
+    o_pre, o_suf, lse_pre, lse_suf = fwd_out
+    return bwd(dev["q_pre"], dev["k_pre"], dev["v_pre"], dev["q_suf"], dev["k_suf"], dev["v_suf"],
+               o_pre, o_suf, lse_pre, lse_suf, dev["do_pre"], dev["do_suf"],
+               dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], dev["scale"])

@@ -1,0 +1,376 @@
+// C ABI of the grouped-attention library (declared in include/pg_attn.h):
+// host-side argument checks, workspace layout, and the launch sequence.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/pg_attn.h"
+#include "pg_bwd.hpp"
+#include "pg_fwd.hpp"
+#include "pg_plan.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+long ceil_div_l(long a, long b) { return (a + b - 1) / b; }
+
+// Workspace layout shared by the forward and backward calls.
+struct Layout {
+  size_t hdr, ginfo, qoff, kvoff, qtiles, qorder, kvtiles, kvorder, seg, dsum, total;
+  long max_q, max_kv;
+};
+
+Layout make_layout(int ng, int ns, int tp, int ts, int h_q, bool bwd) {
+  (void)ns;
+  Layout L{};
+  L.max_q = ceil_div_l(tp, pg::kFwdBM) + ceil_div_l(ts, pg::kFwdBM) + 2L * ng;
+  L.max_kv = bwd ? ceil_div_l(tp, pg::kKvBN) + ceil_div_l(ts, pg::kKvBN) + 2L * ng : 0;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
+  L.hdr = take(sizeof(pg::PlanHeader));
+  L.ginfo = take(sizeof(pg::GroupInfoEx) * (size_t)(ng > 0 ? ng : 1));
+  L.qoff = take(sizeof(int) * (size_t)(ng + 1));
+  L.kvoff = take(sizeof(int) * (size_t)(ng + 1));
+  L.qtiles = take(sizeof(pg::TileDesc) * (size_t)(L.max_q > 0 ? L.max_q : 1));
+  L.qorder = take(sizeof(int) * (size_t)(L.max_q > 0 ? L.max_q : 1));
+  L.kvtiles = take(sizeof(pg::TileDesc) * (size_t)(L.max_kv > 0 ? L.max_kv : 1));
+  L.kvorder = take(sizeof(int) * (size_t)(L.max_kv > 0 ? L.max_kv : 1));
+  L.seg = take(sizeof(int) * (size_t)(ts > 0 ? ts : 1));
+  L.dsum = bwd ? take(sizeof(float) * (size_t)h_q * (size_t)(tp + ts > 0 ? tp + ts : 1)) : off;
+  L.total = off;
+  return L;
+}
+
+
+// ---------------------------------------------------------------- kernel timing
+// Optional HIP-event brackets around each launch, recorded on the launch's own
+// stream. Off unless pg_timing_start() was called.
+namespace timing {
+constexpr int kCap = 16384;
+struct Rec {
+  int kernel;
+  hipEvent_t a, b;
+};
+std::mutex mu;
+bool on = false;
+int n = 0;
+std::vector<Rec> recs;
+
+int begin(int kernel, hipStream_t st) {
+  std::lock_guard<std::mutex> g(mu);
+  if (!on || n >= kCap) return -1;
+  if ((int)recs.size() <= n) {
+    Rec r{kernel, nullptr, nullptr};
+    if (hipEventCreate(&r.a) != hipSuccess || hipEventCreate(&r.b) != hipSuccess) return -1;
+    recs.push_back(r);
+  }
+  recs[n].kernel = kernel;
+  if (hipEventRecord(recs[n].a, st) != hipSuccess) return -1;
+  return n++;
+}
+
+void end(int idx, hipStream_t st) {
+  if (idx < 0) return;
+  std::lock_guard<std::mutex> g(mu);
+  (void)hipEventRecord(recs[idx].b, st);
+}
+}  // namespace timing
+
+struct Timed {
+  int idx;
+  hipStream_t st;
+  Timed(int kernel, hipStream_t s) : idx(timing::begin(kernel, s)), st(s) {}
+  ~Timed() { timing::end(idx, st); }
+};
+
+struct Common {
+  int dtype, ng, ns, tp, ts, h_q, h_kv, d;
+  float scale;
+};
+
+int check_common(const Common& c, const int32_t* cu_p, const int32_t* cu_s, const int32_t* gsz) {
+  if (c.dtype != PG_BF16 && c.dtype != PG_FP32) return fail(PG_EUNSUPPORTED, "dtype %d is not PG_BF16 or PG_FP32", c.dtype);
+  if (c.ng < 0 || c.ns < 0 || c.tp < 0 || c.ts < 0)
+    return fail(PG_EINVAL, "negative size (n_groups=%d n_suffixes=%d total_prefix=%d total_suffix=%d)", c.ng, c.ns,
+                c.tp, c.ts);
+  if (c.ng == 0 && (c.tp != 0 || c.ns != 0)) return fail(PG_EINVAL, "no groups but nonzero prefix rows or members");
+  if (c.ns == 0 && c.ts != 0) return fail(PG_EINVAL, "no members but nonzero total_suffix");
+  if (c.h_q <= 0 || c.h_kv <= 0 || c.h_q % c.h_kv != 0)
+    return fail(PG_EINVAL, "h_q=%d must be a positive multiple of h_kv=%d", c.h_q, c.h_kv);
+  if (c.d != 64 && c.d != 128) return fail(PG_EUNSUPPORTED, "head_dim=%d (supported: 64, 128)", c.d);
+  if (!(std::isfinite(c.scale) && c.scale > 0.f)) return fail(PG_EINVAL, "softmax_scale must be finite and > 0");
+  const long rows = (long)c.tp + c.ts;
+  if (rows * c.h_q > 0x7fffffffL || (long)c.tp * c.h_q * c.d > (1L << 40))
+    return fail(PG_EUNSUPPORTED, "problem too large for 32-bit row*head indexing");
+  if (c.ng > 0 && (!cu_p || !gsz)) return fail(PG_EINVAL, "cu_prefix_lens/group_sizes is NULL");
+  if (c.ns > 0 && !cu_s) return fail(PG_EINVAL, "cu_suffix_lens is NULL");
+  if (c.ng > 0 && !cu_s) return fail(PG_EINVAL, "cu_suffix_lens is NULL");
+  return PG_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(PG_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+int device_ready() {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  return PG_OK;
+}
+
+bool debug_validate() {
+  const char* v = getenv("PG_DEBUG_VALIDATE");
+  return v && v[0] == '1';
+}
+
+// Runs the planner kernels. `bwd` also builds the key/value tile list.
+int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p, const int32_t* cu_s,
+                const int32_t* gsz, hipStream_t st, bool bwd) {
+  Timed tm(PG_K_PLAN, st);
+  auto* hdr = (pg::PlanHeader*)(ws + L.hdr);
+  auto* gi = (pg::GroupInfoEx*)(ws + L.ginfo);
+  int* qoff = (int*)(ws + L.qoff);
+  int* kvoff = (int*)(ws + L.kvoff);
+  hipLaunchKernelGGL(pg::plan_groups_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, cu_p, cu_s, gsz, c.ng, c.ns,
+                     c.tp, c.ts, pg::kFwdBM, pg::kKvBN, L.max_q, bwd ? L.max_kv : 0x7fffffffL, hdr, gi, qoff,
+                     kvoff);
+  auto* qt = (pg::TileDesc*)(ws + L.qtiles);
+  int* qo = (int*)(ws + L.qorder);
+  if (L.max_q > 0) {
+    const int blocks = (int)ceil_div_l(L.max_q, 256);
+    hipLaunchKernelGGL(pg::plan_tiles_kernel, dim3(blocks), dim3(256), 0, st, cu_s, c.ng, pg::kFwdBM, pg::kKvBN,
+                       (int)L.max_q, hdr, gi, qoff, qt, 0);
+    hipLaunchKernelGGL(pg::plan_rank_kernel, dim3(blocks), dim3(256), 0, st, hdr, qt, qo, 0);
+  }
+  if (bwd && L.max_kv > 0) {
+    auto* kt = (pg::TileDesc*)(ws + L.kvtiles);
+    int* ko = (int*)(ws + L.kvorder);
+    const int blocks = (int)ceil_div_l(L.max_kv, 256);
+    hipLaunchKernelGGL(pg::plan_tiles_kernel, dim3(blocks), dim3(256), 0, st, cu_s, c.ng, pg::kFwdBM, pg::kKvBN,
+                       (int)L.max_kv, hdr, gi, kvoff, kt, 1);
+    hipLaunchKernelGGL(pg::plan_rank_kernel, dim3(blocks), dim3(256), 0, st, hdr, kt, ko, 1);
+  }
+  if (c.ts > 0) {
+    hipLaunchKernelGGL(pg::seg_start_kernel, dim3((unsigned)ceil_div_l(c.ts, 256)), dim3(256), 0, st, cu_s, c.ns,
+                       c.ts, hdr, (int*)(ws + L.seg));
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "planner launch");
+  if (debug_validate()) {
+    pg::PlanHeader h;
+    e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "PG_DEBUG_VALIDATE readback");
+    if (h.error) return fail(PG_EINVAL, "grouping arrays are inconsistent (checked on the device)");
+  }
+  return PG_OK;
+}
+
+template <typename T, int D>
+void launch_fwd(const pg::FwdArgs& a, long max_q, hipStream_t st) {
+  const long blocks = max_q * a.h_q;
+  Timed tm(PG_K_FWD, st);
+  if (blocks > 0) hipLaunchKernelGGL((pg::fwd_kernel<T, D>), dim3((unsigned)blocks), dim3(pg::kFwdThreads), 0, st, a);
+}
+
+template <typename T, int D>
+void launch_bwd(const pg::BwdArgs& a, long max_q, long max_kv, hipStream_t st) {
+  const long rows = (long)a.total_prefix + a.total_suffix;
+  if (rows > 0) {
+    const long items = rows * a.h_q;
+    Timed tm(PG_K_BWD_DOT, st);
+    hipLaunchKernelGGL((pg::bwd_dot_kernel<T, D>), dim3((unsigned)ceil_div_l(items, 16)), dim3(256), 0, st, a);
+  }
+  if (max_kv > 0) {
+    Timed tm(PG_K_DKDV, st);
+    hipLaunchKernelGGL((pg::dkdv_kernel<T, D>), dim3((unsigned)(max_kv * a.h_kv)), dim3(pg::kKvThreads), 0, st, a);
+  }
+  if (max_q > 0) {
+    Timed tm(PG_K_DQ, st);
+    hipLaunchKernelGGL((pg::dq_kernel<T, D>), dim3((unsigned)(max_q * a.h_q)), dim3(pg::kDqThreads), 0, st, a);
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t pg_attn_fwd_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q) {
+  if (n_groups < 0 || n_suffixes < 0 || total_prefix < 0 || total_suffix < 0 || h_q < 0) return 0;
+  return make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, false).total;
+}
+
+size_t pg_attn_bwd_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q) {
+  if (n_groups < 0 || n_suffixes < 0 || total_prefix < 0 || total_suffix < 0 || h_q < 0) return 0;
+  return make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, true).total;
+}
+
+const char* pg_status_string(int s) {
+  switch (s) {
+    case PG_OK: return "PG_OK";
+    case PG_EINVAL: return "PG_EINVAL: invalid argument";
+    case PG_EUNSUPPORTED: return "PG_EUNSUPPORTED: unsupported configuration";
+    case PG_EWORKSPACE: return "PG_EWORKSPACE: workspace missing or too small";
+    case PG_EHIP: return "PG_EHIP: HIP runtime error";
+    default: return "unknown pg_status";
+  }
+}
+
+const char* pg_last_error(void) { return g_last_error.c_str(); }
+
+int pg_attn_fwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                int h_q, int h_kv, int head_dim, float softmax_scale,
+                const void* q_pre, const void* k_pre, const void* v_pre,
+                const void* q_suf, const void* k_suf, const void* v_suf,
+                void* o_pre, void* o_suf, float* lse_pre, float* lse_suf,
+                void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  const Common c{dtype, n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, softmax_scale};
+  int rc = check_common(c, cu_prefix_lens, cu_suffix_lens, group_sizes);
+  if (rc) return rc;
+  if (total_prefix > 0 && (!q_pre || !k_pre || !v_pre || !o_pre || !lse_pre))
+    return fail(PG_EINVAL, "a prefix tensor pointer is NULL");
+  if (total_suffix > 0 && (!q_suf || !k_suf || !v_suf || !o_suf || !lse_suf))
+    return fail(PG_EINVAL, "a suffix tensor pointer is NULL");
+  const Layout L = make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, false);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(PG_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
+  if ((rc = device_ready())) return rc;
+  if (n_groups == 0) return PG_OK;
+  hipStream_t st = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  if ((rc = launch_plan(c, L, ws, cu_prefix_lens, cu_suffix_lens, group_sizes, st, false))) return rc;
+  pg::FwdArgs a{};
+  a.q_pre = q_pre; a.k_pre = k_pre; a.v_pre = v_pre; a.q_suf = q_suf; a.k_suf = k_suf; a.v_suf = v_suf;
+  a.o_pre = o_pre; a.o_suf = o_suf; a.lse_pre = lse_pre; a.lse_suf = lse_suf;
+  a.hdr = (const pg::PlanHeader*)(ws + L.hdr);
+  a.ginfo = (const pg::GroupInfoEx*)(ws + L.ginfo);
+  a.qtiles = (const pg::TileDesc*)(ws + L.qtiles);
+  a.qorder = (const int*)(ws + L.qorder);
+  a.seg_start = (const int*)(ws + L.seg);
+  a.h_q = h_q; a.h_kv = h_kv; a.total_prefix = total_prefix; a.total_suffix = total_suffix;
+  a.scale_log2 = softmax_scale * pg::kLog2e;
+  if (dtype == PG_BF16) {
+    if (head_dim == 128) launch_fwd<pg::bf16, 128>(a, L.max_q, st); else launch_fwd<pg::bf16, 64>(a, L.max_q, st);
+  } else {
+    if (head_dim == 128) launch_fwd<float, 128>(a, L.max_q, st); else launch_fwd<float, 64>(a, L.max_q, st);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "forward launch");
+  return PG_OK;
+}
+
+int pg_attn_bwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                int h_q, int h_kv, int head_dim, float softmax_scale,
+                const void* q_pre, const void* k_pre, const void* v_pre,
+                const void* q_suf, const void* k_suf, const void* v_suf,
+                const void* o_pre, const void* o_suf, const float* lse_pre, const float* lse_suf,
+                const void* do_pre, const void* do_suf,
+                void* dq_pre, void* dk_pre, void* dv_pre,
+                void* dq_suf, void* dk_suf, void* dv_suf,
+                void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  const Common c{dtype, n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, softmax_scale};
+  int rc = check_common(c, cu_prefix_lens, cu_suffix_lens, group_sizes);
+  if (rc) return rc;
+  if (total_prefix > 0 && (!q_pre || !k_pre || !v_pre || !o_pre || !lse_pre || !do_pre || !dq_pre || !dk_pre ||
+                           !dv_pre))
+    return fail(PG_EINVAL, "a prefix tensor pointer is NULL");
+  if (total_suffix > 0 && (!q_suf || !k_suf || !v_suf || !o_suf || !lse_suf || !do_suf || !dq_suf || !dk_suf ||
+                           !dv_suf))
+    return fail(PG_EINVAL, "a suffix tensor pointer is NULL");
+  const Layout L = make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, true);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(PG_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
+  if ((rc = device_ready())) return rc;
+  if (n_groups == 0) return PG_OK;
+  hipStream_t st = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  if ((rc = launch_plan(c, L, ws, cu_prefix_lens, cu_suffix_lens, group_sizes, st, true))) return rc;
+  pg::BwdArgs a{};
+  a.q_pre = q_pre; a.k_pre = k_pre; a.v_pre = v_pre; a.q_suf = q_suf; a.k_suf = k_suf; a.v_suf = v_suf;
+  a.o_pre = o_pre; a.o_suf = o_suf; a.do_pre = do_pre; a.do_suf = do_suf;
+  a.lse_pre = lse_pre; a.lse_suf = lse_suf;
+  a.dq_pre = dq_pre; a.dk_pre = dk_pre; a.dv_pre = dv_pre; a.dq_suf = dq_suf; a.dk_suf = dk_suf; a.dv_suf = dv_suf;
+  a.dsum = (float*)(ws + L.dsum);
+  a.hdr = (const pg::PlanHeader*)(ws + L.hdr);
+  a.ginfo = (const pg::GroupInfoEx*)(ws + L.ginfo);
+  a.qtiles = (const pg::TileDesc*)(ws + L.qtiles);
+  a.qorder = (const int*)(ws + L.qorder);
+  a.kvtiles = (const pg::TileDesc*)(ws + L.kvtiles);
+  a.kvorder = (const int*)(ws + L.kvorder);
+  a.seg_start = (const int*)(ws + L.seg);
+  a.h_q = h_q; a.h_kv = h_kv; a.total_prefix = total_prefix; a.total_suffix = total_suffix;
+  a.scale = softmax_scale;
+  a.scale_log2 = softmax_scale * pg::kLog2e;
+  if (dtype == PG_BF16) {
+    if (head_dim == 128) launch_bwd<pg::bf16, 128>(a, L.max_q, L.max_kv, st);
+    else launch_bwd<pg::bf16, 64>(a, L.max_q, L.max_kv, st);
+  } else {
+    if (head_dim == 128) launch_bwd<float, 128>(a, L.max_q, L.max_kv, st);
+    else launch_bwd<float, 64>(a, L.max_q, L.max_kv, st);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "backward launch");
+  return PG_OK;
+}
+
+int pg_timing_start(void) {
+  std::lock_guard<std::mutex> g(timing::mu);
+  timing::on = true;
+  timing::n = 0;
+  return PG_OK;
+}
+
+int pg_timing_stop(void) {
+  std::lock_guard<std::mutex> g(timing::mu);
+  timing::on = false;
+  return PG_OK;
+}
+
+int pg_timing_get(int kernel, int* launches, double* total_ms) {
+  if (!launches || !total_ms) return fail(PG_EINVAL, "NULL output pointer");
+  std::lock_guard<std::mutex> g(timing::mu);
+  int cnt = 0;
+  double tot = 0.0;
+  for (int i = 0; i < timing::n; ++i) {
+    const timing::Rec& r = timing::recs[i];
+    if (r.kernel != kernel) continue;
+    hipError_t e = hipEventSynchronize(r.b);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess) return hip_fail(e, "timing event");
+    ++cnt;
+    tot += ms;
+  }
+  *launches = cnt;
+  *total_ms = tot;
+  return PG_OK;
+}
+
+}  // extern "C"

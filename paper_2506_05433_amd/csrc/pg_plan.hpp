@@ -1,0 +1,207 @@
+// Device-side planner: validates the grouping arrays and builds the tile lists
+// that the attention kernels walk, ordered longest-first.
+//
+// Query tiles follow the two attention calls of Eq. (4): prefix query tiles
+// (causal self-attention over the prefix) and response query tiles. Response
+// rows of all members of a group are stacked into common tiles: every one of
+// them sees the whole group prefix, so the prefix part of a tile is a dense
+// rectangle regardless of member boundaries, and only the response part needs
+// the per-member causal mask. Key/value tiles are the mirror image for the
+// key-stationary gradient kernel.
+#pragma once
+#include "pg_common.hpp"
+
+namespace pg {
+
+struct PlanHeader {
+  int error;     // nonzero when the grouping arrays are inconsistent
+  int n_qtiles;  // number of query tiles
+  int n_kvtiles; // number of key/value tiles
+  int pad[61];
+};
+
+struct GroupInfoEx {
+  int p0, p1, s0, s1, m0, m1, pad0, pad1;
+};
+
+// Inclusive scan of one value per thread over a block of NT threads.
+template <int NT>
+__device__ __forceinline__ int block_inclusive_scan(int v, int* tmp) {
+  const int t = threadIdx.x;
+  tmp[t] = v;
+  __syncthreads();
+  for (int off = 1; off < NT; off <<= 1) {
+    int add = (t >= off) ? tmp[t - off] : 0;
+    __syncthreads();
+    tmp[t] += add;
+    __syncthreads();
+  }
+  int r = tmp[t];
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Largest index i in [lo, hi) with a[i] <= x (a nondecreasing, a[lo] <= x).
+__device__ __forceinline__ int upper_index(const int* a, int lo, int hi, int x) {
+  while (hi - lo > 1) {
+    int mid = (lo + hi) >> 1;
+    if (a[mid] <= x) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+constexpr int kPlanThreads = 1024;
+
+// One block. Validates and computes per-group ranges and tile offsets.
+__global__ void __launch_bounds__(kPlanThreads) plan_groups_kernel(
+    const int* __restrict__ cu_p, const int* __restrict__ cu_s, const int* __restrict__ gsz,
+    int ng, int ns, int tp, int ts, int bm, int bkv, long max_q, long max_kv,
+    PlanHeader* hdr, GroupInfoEx* ginfo, int* qoff, int* kvoff) {
+  __shared__ int tmp[kPlanThreads];
+  __shared__ int err;
+  __shared__ int carry[3];
+  const int t = threadIdx.x;
+  if (t == 0) { err = 0; carry[0] = carry[1] = carry[2] = 0; }
+  __syncthreads();
+  int bad = 0;
+  for (int g = t; g <= ng; g += kPlanThreads) {
+    int v = cu_p[g];
+    if (g == 0 && v != 0) bad = 1;
+    if (g == ng && v != tp) bad = 1;
+    if (g > 0 && v < cu_p[g - 1]) bad = 1;
+    if (g < ng && gsz[g] < 0) bad = 1;
+  }
+  for (int m = t; m <= ns; m += kPlanThreads) {
+    int v = cu_s[m];
+    if (m == 0 && v != 0) bad = 1;
+    if (m == ns && v != ts) bad = 1;
+    if (m > 0 && v < cu_s[m - 1]) bad = 1;
+  }
+  if (bad) atomicOr(&err, 1);
+  __syncthreads();
+  // member starts: exclusive scan of group sizes (checked against ns afterwards)
+  for (int base = 0; base < ng; base += kPlanThreads) {
+    const int g = base + t;
+    const int v = (g < ng && !err) ? gsz[g] : 0;
+    const int inc = block_inclusive_scan<kPlanThreads>(v, tmp);
+    if (g < ng) { ginfo[g].m0 = carry[0] + inc - v; ginfo[g].m1 = carry[0] + inc; }
+    __syncthreads();
+    if (t == kPlanThreads - 1) carry[0] += inc;
+    __syncthreads();
+  }
+  if (t == 0 && carry[0] != ns) err = 1;
+  __syncthreads();
+  const int ok = !err;
+  for (int base = 0; base < ng; base += kPlanThreads) {
+    const int g = base + t;
+    int nq = 0, nkv = 0;
+    if (g < ng && ok) {
+      GroupInfoEx gi = ginfo[g];
+      gi.p0 = cu_p[g]; gi.p1 = cu_p[g + 1];
+      gi.s0 = cu_s[gi.m0]; gi.s1 = cu_s[gi.m1];
+      gi.pad0 = gi.pad1 = 0;
+      ginfo[g] = gi;
+      nq = ceil_div(gi.p1 - gi.p0, bm) + ceil_div(gi.s1 - gi.s0, bm);
+      nkv = ceil_div(gi.p1 - gi.p0, bkv) + ceil_div(gi.s1 - gi.s0, bkv);
+    }
+    const int iq = block_inclusive_scan<kPlanThreads>(nq, tmp);
+    const int ikv = block_inclusive_scan<kPlanThreads>(nkv, tmp);
+    if (g < ng) { qoff[g] = carry[1] + iq - nq; kvoff[g] = carry[2] + ikv - nkv; }
+    __syncthreads();
+    if (t == kPlanThreads - 1) { carry[1] += iq; carry[2] += ikv; }
+    __syncthreads();
+  }
+  // the host sized the tile arrays from the totals; a list longer than that bound
+  // can only come from inconsistent arrays, so it is treated as an error too
+  if (t == 0 && ok && (carry[1] > max_q || carry[2] > max_kv)) err = 1;
+  __syncthreads();
+  if (t == 0) {
+    const int ok = !err;
+    qoff[ng] = ok ? carry[1] : 0;
+    kvoff[ng] = ok ? carry[2] : 0;
+    hdr->error = err;
+    hdr->n_qtiles = ok ? carry[1] : 0;
+    hdr->n_kvtiles = ok ? carry[2] : 0;
+  }
+}
+
+// One thread per (possible) tile: fills the descriptors. `which` 0 = query tiles, 1 = kv tiles.
+__global__ void plan_tiles_kernel(const int* __restrict__ cu_s, int ng, int bm, int bkv, int max_tiles,
+                                  const PlanHeader* hdr, const GroupInfoEx* __restrict__ ginfo,
+                                  const int* __restrict__ off, TileDesc* tiles, int which) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int n = which ? hdr->n_kvtiles : hdr->n_qtiles;
+  if (i >= n || i >= max_tiles) return;
+  const int g = upper_index(off, 0, ng, i);  // off[ng] == n > i, groups with no tile share offsets
+  // skip groups with zero tiles that share the offset of the next one
+  const GroupInfoEx gi = ginfo[g];
+  const int b = which ? bkv : bm;
+  const int local = i - off[g];
+  const int np = ceil_div(gi.p1 - gi.p0, b);
+  TileDesc d;
+  d.group = g;
+  d.pad0 = d.pad1 = 0;
+  if (local < np) {
+    d.kind = 0;
+    d.row0 = gi.p0 + local * b;
+    d.row1 = min(d.row0 + b, gi.p1);
+    if (!which) {
+      d.aux = 0;
+      d.work = d.row1 - gi.p0;                          // keys seen by the last row
+    } else {
+      d.aux = 0;
+      d.work = (gi.p1 - d.row0) + (gi.s1 - gi.s0);      // query rows that see these keys
+    }
+  } else {
+    d.kind = 1;
+    d.row0 = gi.s0 + (local - np) * b;
+    d.row1 = min(d.row0 + b, gi.s1);
+    if (!which) {
+      const int m = upper_index(cu_s, gi.m0, gi.m1, d.row0);
+      d.aux = cu_s[m];                                  // first response key of the tile
+      d.work = (gi.p1 - gi.p0) + (d.row1 - d.aux);
+    } else {
+      const int m = upper_index(cu_s, gi.m0, gi.m1, d.row1 - 1);
+      d.aux = cu_s[m + 1];                              // end of queries that see the keys
+      d.work = d.aux - d.row0;
+    }
+  }
+  tiles[i] = d;
+}
+
+// Longest-first order: order[rank] = tile, rank by (work desc, index asc). Deterministic.
+__global__ void __launch_bounds__(256) plan_rank_kernel(const PlanHeader* hdr, const TileDesc* __restrict__ tiles,
+                                                        int* order, int which) {
+  __shared__ int w[1024];
+  const int n = which ? hdr->n_kvtiles : hdr->n_qtiles;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if ((int)(blockIdx.x * blockDim.x) >= n) return;
+  const int mine = i < n ? tiles[i].work : 0;
+  int rank = 0;
+  for (int base = 0; base < n; base += 1024) {
+    __syncthreads();
+    for (int k = threadIdx.x; k < 1024; k += blockDim.x) w[k] = (base + k < n) ? tiles[base + k].work : -1;
+    __syncthreads();
+    if (i < n) {
+      const int lim = min(1024, n - base);
+      for (int k = 0; k < lim; ++k) {
+        const int o = w[k];
+        rank += (o > mine) || (o == mine && base + k < i);
+      }
+    }
+  }
+  if (i < n) order[rank] = i;
+}
+
+// seg_start[r] = first row of the member that owns response row r.
+__global__ void seg_start_kernel(const int* __restrict__ cu_s, int ns, int ts, const PlanHeader* hdr,
+                                 int* seg_start) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= ts || hdr->error) return;
+  const int m = upper_index(cu_s, 0, ns, r);
+  seg_start[r] = cu_s[m];
+}
+
+}  // namespace pg

@@ -1,0 +1,77 @@
+"""Helpers for GPU-vs-oracle parity tests (tolerances written here, once).
+
+Tolerances (per tensor):
+* fp32 workloads: max |gpu - oracle| <= 1e-4 for outputs, log-sum-exp and gradients;
+* bf16 workloads: outputs and log-sum-exp max |gpu - oracle| <= 2e-2; gradients
+  max |gpu - oracle| / max |oracle| <= 3e-2.
+The oracle runs in float64 on exactly the (bf16-rounded) inputs the GPU sees.
+"""
+import sys
+
+import numpy as np
+
+from paper_2506_05433_amd.inputs import bf16_bits_to_f32
+
+FP32_ABS = 1e-4
+BF16_OUT_ABS = 2e-2
+BF16_GRAD_REL = 3e-2
+
+OUTS = ("o_pre", "o_suf", "lse_pre", "lse_suf")
+GRADS = ("dq_pre", "dk_pre", "dv_pre", "dq_suf", "dk_suf", "dv_suf")
+
+
+class Bf16View:
+    """Read-only view of bf16 bit patterns that decodes exactly to float32 on indexing."""
+
+    def __init__(self, bits):
+        self.bits = bits
+        self.shape = bits.shape
+
+    def __getitem__(self, idx):
+        return bf16_bits_to_f32(np.asarray(self.bits[idx]))
+
+    def __array__(self, dtype=None, copy=None):
+        a = bf16_bits_to_f32(self.bits)
+        return a if dtype is None else a.astype(dtype)
+
+
+def host_view(prob):
+    """The problem's tensors as arrays/views the oracle can index (values exactly as on the GPU)."""
+    out = {}
+    for k, a in prob.tensors.items():
+        out[k] = Bf16View(a) if a.dtype == np.uint16 else a
+    return out
+
+
+def to_host(t):
+    import torch
+    return t.detach().float().cpu().numpy() if t.dtype != torch.float32 else t.detach().cpu().numpy()
+
+
+def report(name, got, ref):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if ref.size == 0:
+        return 0.0, 0.0
+    err = float(np.abs(got - ref).max())
+    scale = float(np.abs(ref).max())
+    return err, err / scale if scale > 0 else err
+
+
+def check(name, got, ref, dtype, log=None):
+    """Assert ``got`` matches ``ref`` under the tolerance for tensor ``name`` in ``dtype`` mode."""
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), f"{name}: non-finite values"
+    err, rel = report(name, got, ref)
+    grad = name.startswith("d")
+    if dtype == "fp32":
+        ok, bound, val = err <= FP32_ABS, FP32_ABS, err
+    elif grad:
+        ok, bound, val = rel <= BF16_GRAD_REL, BF16_GRAD_REL, rel
+    else:
+        ok, bound, val = err <= BF16_OUT_ABS, BF16_OUT_ABS, err
+    msg = f"{name}: max_abs={err:.3e} max_rel={rel:.3e} (bound {bound:g})"
+    if log is not None:
+        log.append(msg)
+    print(msg, file=sys.stderr)
+    assert ok, msg

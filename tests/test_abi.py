@@ -1,0 +1,94 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared
+symbol, sizes its workspace, and rejects bad arguments on the host before
+anything is launched."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2506_05433_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pg_attn.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pg_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_expected_entry_points():
+    assert set(declared_functions()) == set(binding.SIGNATURES)
+
+
+def test_library_exports_every_declared_symbol():
+    L = binding.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_status_strings():
+    L = binding.lib()
+    for s, tag in binding.STATUS.items():
+        assert L.pg_status_string(s).decode().startswith(tag)
+
+
+def test_workspace_sizes_grow_with_the_problem():
+    f1 = binding.workspace_bytes("fwd", 1, 8, 4096, 5120, 32)
+    b1 = binding.workspace_bytes("bwd", 1, 8, 4096, 5120, 32)
+    f2 = binding.workspace_bytes("fwd", 8, 128, 73275, 266240, 64)
+    assert 0 < f1 < b1 and f1 < f2
+    # the backward workspace holds rowsum(dO*O): h_q * rows floats
+    assert b1 >= 32 * (4096 + 5120) * 4
+    assert binding.workspace_bytes("fwd", -1, 0, 0, 0, 1) == 0
+
+
+def _call_fwd(**over):
+    args = dict(dtype=0, ng=1, ns=2, tp=8, ts=6, cu_p=1, cu_s=1, gsz=1, h_q=4, h_kv=2, d=128, scale=0.125,
+                ptr=1, ws=1, ws_bytes=1 << 30)
+    args.update(over)
+    p = lambda v: ctypes.c_void_p(v) if v else None  # noqa: E731
+    L = binding.lib()
+    return L.pg_attn_fwd(args["dtype"], args["ng"], args["ns"], args["tp"], args["ts"],
+                         p(args["cu_p"]), p(args["cu_s"]), p(args["gsz"]), args["h_q"], args["h_kv"], args["d"],
+                         args["scale"], *[p(args["ptr"])] * 10, p(args["ws"]), args["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(dtype=7), 2),
+    (dict(d=96), 2),
+    (dict(h_q=6, h_kv=4), 1),
+    (dict(h_kv=0), 1),
+    (dict(scale=float("nan")), 1),
+    (dict(scale=-1.0), 1),
+    (dict(tp=-3), 1),
+    (dict(ng=0), 1),
+    (dict(ns=0), 1),
+    (dict(cu_p=0), 1),
+    (dict(cu_s=0), 1),
+    (dict(ptr=0), 1),
+    (dict(ws=0), 3),
+    (dict(ws_bytes=16), 3),
+])
+def test_host_validation_rejects_before_launch(over, status):
+    """Bad arguments are rejected on the host (no pointer is dereferenced, nothing launches)."""
+    assert _call_fwd(**over) == status
+    assert binding.lib().pg_last_error().decode() != ""
+
+
+def test_bwd_validation():
+    L = binding.lib()
+    p = ctypes.c_void_p(1)
+    st = L.pg_attn_bwd(0, 1, 2, 8, 6, p, p, p, 4, 2, 64, 0.125, *[p] * 18, p, 16, None)
+    assert st == 3
+
+
+def test_valid_call_without_a_gpu_reports_hip_error():
+    """With no usable device the call fails with PG_EHIP instead of crashing (host-forced failure path)."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    assert _call_fwd() == 4
+    assert "hip" in binding.lib().pg_last_error().decode().lower()

@@ -1,0 +1,222 @@
+"""GPU parity: the HIP library against the CPU oracle on the same seeded inputs.
+
+Small problems are compared element by element on every output and gradient;
+the five workloads are compared at full size in the launch configuration the
+bench uses, either on every element of a subset of heads (single_group) or on
+sampled query rows and keys the oracle computes one by one.
+"""
+import os
+
+import numpy as np
+import pytest
+
+from oracle import grouped_oracle, key_gradients, query_rows
+from paper_2506_05433_amd.inputs import make_problem
+from tests._parity import GRADS, OUTS, check, host_view, to_host
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _dev():
+    from paper_2506_05433_amd import binding
+    assert torch.cuda.is_available(), "GPU test needs a GPU"
+    binding.lib()
+    return binding
+
+
+def _run(prob, grads=True):
+    binding = _dev()
+    dev = binding.to_device(prob, "cuda")
+    f = binding.run_fwd(dev)
+    res = dict(zip(OUTS, f))
+    if grads:
+        res.update(zip(GRADS, binding.run_bwd(dev, f)))
+    torch.cuda.synchronize()
+    return {k: to_host(v) for k, v in res.items()}
+
+
+def _oracle(prob, grads, heads):
+    """Full oracle; with ``heads``, one thread per query head (numpy releases the GIL), results merged."""
+    t = host_view(prob)
+    args = (prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
+    if heads is None:
+        return grouped_oracle(*args, t, prob.scale, grads=grads)
+    from concurrent.futures import ThreadPoolExecutor
+    tf = {k: np.asarray(v, np.float64) for k, v in t.items()}
+    with ThreadPoolExecutor(len(heads)) as ex:
+        parts = list(ex.map(lambda h: grouped_oracle(*args, tf, prob.scale, grads=grads, heads=[h]), heads))
+    ref = {k: (sum(p[k] for p in parts) if k in ("dk_pre", "dk_suf", "dv_pre", "dv_suf", "prefix_member_spread")
+               else None) for k in parts[0]}
+    for k in parts[0]:
+        if ref[k] is None:
+            ref[k] = parts[0][k].copy()
+            for h, p in zip(heads, parts):
+                if k.startswith("lse"):
+                    ref[k][h] = p[k][h]
+                else:
+                    ref[k][:, h] = p[k][:, h]
+    return ref
+
+
+def _full_compare(prob, grads=True, heads=None, kv_heads=None):
+    print(f"[parity] {prob.workload.name} seed={prob.seed} P={list(prob.prefix_lens)} G={list(prob.group_sizes)} "
+          f"S={list(prob.suffix_lens)[:8]}... hq={prob.h_q} hkv={prob.h_kv} d={prob.head_dim} {prob.dtype}",
+          flush=True)
+    got = _run(prob, grads)
+    ref = _oracle(prob, grads, heads)
+    assert ref["prefix_member_spread"] == 0.0
+    hs = slice(None) if heads is None else list(heads)
+    for k in OUTS:
+        if k.startswith("lse"):
+            check(k, got[k][hs], ref[k][hs], prob.dtype)
+        else:
+            check(k, got[k][:, hs], ref[k][:, hs], prob.dtype)
+    if grads:
+        ks = slice(None) if kv_heads is None else list(kv_heads)
+        for k in GRADS:
+            sel = hs if k.startswith("dq") else ks
+            check(k, got[k][:, sel], ref[k][:, sel], prob.dtype)
+    return got
+
+
+def test_tiny_fp32_workload():
+    """The 'tiny' workload (fp32, d=64) element by element."""
+    _full_compare(make_problem("tiny", seed=0))
+
+
+SMALL = [
+    # (lengths, h_q, h_kv, d, dtype): several tiles, ragged tails, GQA ratios 1/4/5/8, edge sizes
+    (((300,), (5,), (130, 1, 64, 200, 97)), 8, 2, 128, "bf16"),
+    (((257, 0, 40), (3, 2, 0), (129, 128, 1, 300, 0)), 5, 1, 128, "bf16"),
+    (((1000,), (4,), (70, 250, 33, 190)), 8, 1, 128, "bf16"),
+    (((190,), (3,), (64, 65, 127)), 4, 4, 64, "bf16"),
+    (((513, 77), (2, 3), (200, 5, 64, 1, 300)), 4, 2, 64, "bf16"),
+    (((300,), (5,), (130, 1, 64, 200, 97)), 4, 2, 128, "fp32"),
+    (((129, 0), (2, 2), (40, 63, 1, 128)), 2, 1, 64, "fp32"),
+    (((0,), (1,), (5,)), 2, 2, 64, "bf16"),
+    (((7,), (0,), ()), 2, 1, 128, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SMALL)))
+def test_small_full(case):
+    lengths, hq, hkv, d, dt = SMALL[case]
+    prob = make_problem("single_group", seed=100 + case, lengths=lengths, h_q=hq, h_kv=hkv, head_dim=d, dtype=dt,
+                        scale=1.0 / np.sqrt(d))
+    _full_compare(prob)
+
+
+def test_peaked_softmax_rescaling():
+    """Q x 4: sharp rows exercise the running-max rescale of the online softmax."""
+    prob = make_problem("single_group", seed=7, lengths=((700,), (3,), (300, 90, 211)), h_q=4, h_kv=1,
+                        head_dim=128, peaked=True)
+    _full_compare(prob)
+
+
+def test_single_group_workload_kv_head0():
+    """single_group (P=4096, G=8, 32/8 heads) at full size; every element of query heads 0-3 and kv head 0."""
+    prob = make_problem("single_group", seed=0)
+    _full_compare(prob, heads=[0, 1, 2, 3], kv_heads=[0])
+
+
+def _sampled_compare(prob, n_rows=12, n_keys=6, heads=None, kv_head=0, group=0, seed=0):
+    print(f"[parity] sampled {prob.workload.name} seed={prob.seed} total_prefix={prob.total_prefix} "
+          f"total_suffix={prob.total_suffix}", flush=True)
+    got = _run(prob)
+    t = host_view(prob)
+    rng = np.random.default_rng(seed)
+    hq = prob.h_q
+    heads = heads if heads is not None else [0, hq // 2 + 1, hq - 1]
+    cu_p, cu_s = prob.cu_prefix, prob.cu_suffix
+    pre_rows = sorted(set([0, 127, 128, int(cu_p[1]) - 1] + list(rng.integers(0, prob.total_prefix, n_rows))))
+    suf_rows = sorted(set([0, int(cu_s[1]) - 1, int(cu_s[1]), prob.total_suffix - 1] +
+                          list(rng.integers(0, prob.total_suffix, n_rows))))
+    for side, rows in (("pre", pre_rows), ("suf", suf_rows)):
+        r = query_rows(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, side, rows, heads)
+        check("o_" + side, got["o_" + side][rows][:, heads], r["o"], prob.dtype)
+        check("lse_" + side, got["lse_" + side][heads][:, rows], r["lse"], prob.dtype)
+        check("dq_" + side, got["dq_" + side][rows][:, heads], r["dq"], prob.dtype)
+    p0, p1 = int(cu_p[group]), int(cu_p[group + 1])
+    m0 = int(prob.group_sizes[:group].sum())
+    m1 = m0 + int(prob.group_sizes[group])
+    pkeys = sorted(set([p0, p1 - 1, min(p0 + 128, p1 - 1)] + list(rng.integers(p0, p1, n_keys))))
+    skeys = sorted(set([int(cu_s[m0]), int(cu_s[m1]) - 1] + list(rng.integers(cu_s[m0], cu_s[m1], n_keys))))
+    for side, keys in (("pre", pkeys), ("suf", skeys)):
+        r = key_gradients(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, group, kv_head, side,
+                          keys)
+        # relative bound against the sampled reference's own max, plus the full tensor's scale
+        check("dk_" + side, got["dk_" + side][keys, kv_head], r["dk"], prob.dtype)
+        check("dv_" + side, got["dv_" + side][keys, kv_head], r["dv"], prob.dtype)
+    # identities over every key of group 0 / kv head 0 (any size): sum dK = 0, sum dV = sum dO
+    s0, s1 = int(cu_s[m0]), int(cu_s[m1])
+    hs = [h for h in range(hq) if h // (hq // prob.h_kv) == kv_head]
+    dv_sum = got["dv_pre"][p0:p1, kv_head].astype(np.float64).sum(0) + got["dv_suf"][s0:s1, kv_head].sum(0)
+    do_sum = np.asarray(t["do_pre"][p0:p1], np.float64)[:, hs].sum((0, 1)) + \
+        np.asarray(t["do_suf"][s0:s1], np.float64)[:, hs].sum((0, 1))
+    rel = np.abs(dv_sum - do_sum).max() / np.abs(do_sum).max()
+    print(f"sum dV vs sum dO rel={rel:.3e}", flush=True)
+    assert rel < 3e-2
+
+
+def test_long_prefix_workload_sampled():
+    _sampled_compare(make_problem("long_prefix", seed=0))
+
+
+def test_large_group_workload_sampled():
+    _sampled_compare(make_problem("large_group", seed=0))
+
+
+def test_packed_varlen_workload_sampled():
+    prob = make_problem("packed_varlen", seed=0)
+    g = int(np.argmin(prob.prefix_lens))
+    _sampled_compare(prob, group=g, kv_head=3)
+
+
+def test_deterministic():
+    """Two runs on identical inputs are bitwise equal (fixed-order reductions, no atomics)."""
+    prob = make_problem("single_group", seed=3, lengths=((900,), (6,), (100, 300, 1, 250, 64, 129)), h_q=8, h_kv=2,
+                        head_dim=128)
+    a = _run(prob)
+    b = _run(prob)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
+def test_repeated_layout_sums_to_grouped():
+    """The same kernels on the repeated-prefix layout give the grouped results (Lemma 1 on the GPU)."""
+    from paper_2506_05433_amd.inputs import repeated_layout
+    prob = make_problem("single_group", seed=4, lengths=((520,), (3,), (100, 7, 260)), h_q=4, h_kv=1, head_dim=128,
+                        dtype="fp32")
+    rep = repeated_layout(prob)
+    g = _run(prob)
+    r = _run(rep)
+    P = int(prob.prefix_lens[0])
+    np.testing.assert_allclose(r["o_suf"], g["o_suf"], atol=1e-5)
+    for i in range(3):
+        np.testing.assert_allclose(r["o_pre"][i * P:(i + 1) * P], g["o_pre"], atol=1e-5)
+    for name in ("dk_pre", "dv_pre", "dq_pre"):
+        s = sum(r[name][i * P:(i + 1) * P] for i in range(3))
+        np.testing.assert_allclose(s, g[name], atol=1e-4)
+
+
+def test_invalid_grouping_arrays_do_no_work(monkeypatch):
+    """Inconsistent device grouping arrays: nothing is computed, and PG_DEBUG_VALIDATE=1 reports PG_EINVAL."""
+    binding = _dev()
+    prob = make_problem("single_group", seed=5, lengths=((64,), (2,), (10, 20)), h_q=2, h_kv=1, head_dim=64)
+    dev = binding.to_device(prob, "cuda")
+    dev["cu_suffix"] = torch.tensor([0, 25, 20], dtype=torch.int32, device="cuda")  # not nondecreasing
+    o_pre = torch.full_like(dev["q_pre"], 7.0)
+    o_suf = torch.full_like(dev["q_suf"], 7.0)
+    lp = torch.zeros(2, 64, device="cuda")
+    ls = torch.zeros(2, 30, device="cuda")
+    binding.fwd(dev["q_pre"], dev["k_pre"], dev["v_pre"], dev["q_suf"], dev["k_suf"], dev["v_suf"],
+                dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], dev["scale"], out=(o_pre, o_suf, lp, ls))
+    torch.cuda.synchronize()
+    assert bool((o_pre == 7.0).all()) and bool((o_suf == 7.0).all())
+    monkeypatch.setenv("PG_DEBUG_VALIDATE", "1")
+    with pytest.raises(binding.PgError) as e:
+        binding.fwd(dev["q_pre"], dev["k_pre"], dev["v_pre"], dev["q_suf"], dev["k_suf"], dev["v_suf"],
+                    dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], dev["scale"])
+    assert e.value.status == 1
