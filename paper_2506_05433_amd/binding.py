@@ -11,7 +11,8 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libpg_attn.so")
+# PG_LIB overrides the library file (used to compare builds of the same sources)
+LIB_PATH = os.environ.get("PG_LIB") or os.path.join(HERE, "libpg_attn.so")
 
 PG_BF16, PG_FP32 = 0, 1
 STATUS = {0: "PG_OK", 1: "PG_EINVAL", 2: "PG_EUNSUPPORTED", 3: "PG_EWORKSPACE", 4: "PG_EHIP"}

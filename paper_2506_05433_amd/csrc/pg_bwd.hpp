@@ -16,6 +16,8 @@
 //         from the accumulators as B operands and dO^T, Q^T through transposing LDS reads.
 //   dq  : S^T = K Q^T and dP^T = V dO^T with queries as columns; dQ^T += K^T dS^T.
 #pragma once
+#include <type_traits>
+
 #include "pg_common.hpp"
 #include "pg_plan.hpp"
 
@@ -69,8 +71,7 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
   using Frag = typename E::Frag;
   constexpr int BQ = kKvBQ;
   constexpr int KK = D / 16, DB = D / 32;
-  constexpr int PITCH = D * (int)sizeof(T) + 16;
-  constexpr int TILE = BQ * PITCH;
+  constexpr int TILE = LdsTile<T, D>::bytes(BQ);
   __shared__ __attribute__((aligned(16))) char smem[2][2][TILE];  // [buffer][Q, dO]
   __shared__ __attribute__((aligned(16))) float s_lse[2][BQ];     // lse * log2(e), +inf for padding
   __shared__ __attribute__((aligned(16))) float s_dsum[2][BQ];
@@ -85,7 +86,7 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
   const int ratio = a.h_q / a.h_kv;
   const int rows_all = a.total_prefix + a.total_suffix;
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, wave = uniform(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hh = lane >> 5;
   const int wk0 = td.row0 + 32 * wave;            // first key of this wave
   const bool wave_active = wk0 < td.row1;
@@ -149,8 +150,8 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
     }
   };
   auto commit = [&](int buf) {
-    ldq.store(smem[buf][0], PITCH, tid);
-    ldo.store(smem[buf][1], PITCH, tid);
+    ldq.store(smem[buf][0], tid);
+    ldo.store(smem[buf][1], tid);
     if (tid < BQ) { s_lse[buf][tid] = pf_lse; s_dsum[buf][tid] = pf_dsum; s_seg[buf][tid] = pf_seg; }
   };
 
@@ -167,7 +168,7 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
     const int qend = first ? r1_hi : r2_hi;
     // masking mode: causal when queries and keys are on the same side
     const bool causal = first;  // prefix keys x prefix rows, or response keys x response rows
-    bool skip = false, full = q0 + BQ <= qend;
+    bool skip = false, full = true;  // padding rows need no mask: their lse is +inf
     if (causal) {
       skip = q0 + BQ - 1 < wk0;                      // every query precedes every key
       full = full && (q0 >= wk1);                    // every query sees every key
@@ -182,52 +183,53 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
     if (wave_active && !skip) {
       const char* Qt = smem[buf][0];
       const char* Gt = smem[buf][1];
-      f32x16 s[2], dp[2];
+      // two halves of 32 query rows, one after the other (keeps S and dP of 32 rows live)
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
-        s[qb] = f32x16{};
-        dp[qb] = f32x16{};
-        const char* qrow = Qt + (32 * qb + n) * PITCH + 8 * hh * (int)sizeof(T);
-        const char* grow = Gt + (32 * qb + n) * PITCH + 8 * hh * (int)sizeof(T);
+        f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
-          s[qb] = E::mma(E::lds_row(qrow + 16 * kk * (int)sizeof(T)), kf[kk], s[qb]);
-          dp[qb] = E::mma(E::lds_row(grow + 16 * kk * (int)sizeof(T)), vf[kk], dp[qb]);
+          s = E::mma(E::template lds_row<D>(Qt, 32 * qb + n, 2 * kk + hh), kf[kk], s);
+          dp = E::mma(E::template lds_row<D>(Gt, 32 * qb + n, 2 * kk + hh), vf[kk], dp);
         }
-      }
-      // P = exp2(S*c - lse2), dS = P * (dP - Dsum); rows are queries, lane column is the key
+        // P = exp2(S*c - lse*log2e) (0 on padding rows, whose lse is +inf);
+        // dS = P * (dP - Dsum); rows are queries, the lane's column is its key.
+        // The mask is only evaluated on tiles that straddle a boundary, branch-free.
+        auto softmax_grad = [&](auto masked) {
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
+          for (int i = 0; i < 4; ++i) {
+            const int qi = 32 * qb + 8 * i + 4 * hh;
+            const f32x4 l4 = *(const f32x4*)&s_lse[buf][qi];
+            const f32x4 d4 = *(const f32x4*)&s_dsum[buf][qi];
+            int4 g4 = int4{0, 0, 0, 0};
+            if (decltype(masked)::value) g4 = *(const int4*)&s_seg[buf][qi];
+            const int gs[4] = {g4.x, g4.y, g4.z, g4.w};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int qi = 32 * qb + 8 * i + 4 * hh;
-          const f32x4 l4 = *(const f32x4*)&s_lse[buf][qi];
-          const f32x4 d4 = *(const f32x4*)&s_dsum[buf][qi];
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
-            const int r = 4 * i + jj;
-            float p = fast_exp2(s[qb][r] * c - l4[jj]);
-            if (!full) {
-              const int q = q0 + qi + jj;
-              bool ok = (q < qend);
-              if (causal) ok = ok && (key_c <= q);
-              if (causal && kv_suffix) ok = ok && (key_c >= s_seg[buf][qi + jj]);
-              p = ok ? p : 0.f;
+            for (int jj = 0; jj < 4; ++jj) {
+              const int r = 4 * i + jj;
+              float p = fast_exp2(fmaf(s[r], c, -l4[jj]));
+              if (decltype(masked)::value) {
+                const int q = q0 + qi + jj;
+                const bool ok = (key_c <= q) & (key_c >= gs[jj]);
+                p = ok ? p : 0.f;
+              }
+              s[r] = p;
+              dp[r] = p * (dp[r] - d4[jj]);
             }
-            s[qb][r] = p;
-            dp[qb][r] = p * (dp[qb][r] - d4[jj]);
           }
-        }
-      }
-      // dV^T += dO^T P ; dK^T += Q^T dS   (k = the 64 queries in 4 steps)
+        };
+        if (full) softmax_grad(std::false_type{}); else softmax_grad(std::true_type{});
+        // dV^T += dO^T P ; dK^T += Q^T dS over these 32 queries (two k steps of 16)
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const Frag pfr = E::acc_to_frag(s[t >> 1], t & 1);
-        const Frag dsf = E::acc_to_frag(dp[t >> 1], t & 1);
+        for (int t2 = 0; t2 < 2; ++t2) {
+          const int t = 2 * qb + t2;
+          const Frag pfr = E::acc_to_frag(s, t2);
+          const Frag dsf = E::acc_to_frag(dp, t2);
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          dv[db] = E::mma(E::lds_tr(Gt, PITCH, 16 * t, 32 * db, lane), pfr, dv[db]);
-          dk[db] = E::mma(E::lds_tr(Qt, PITCH, 16 * t, 32 * db, lane), dsf, dk[db]);
+          for (int db = 0; db < DB; ++db) {
+            dv[db] = E::mma(E::template lds_tr<D>(Gt, 16 * t, 32 * db, lane), pfr, dv[db]);
+            dk[db] = E::mma(E::template lds_tr<D>(Qt, 16 * t, 32 * db, lane), dsf, dk[db]);
+          }
         }
       }
     }
@@ -255,13 +257,15 @@ constexpr int kDqBN = 64;
 constexpr int kDqThreads = 256;
 
 template <typename T, int D>
-__global__ void __launch_bounds__(kDqThreads) dq_kernel(const BwdArgs a) {
+#ifndef PG_DQ_MIN_BLOCKS
+#define PG_DQ_MIN_BLOCKS 2
+#endif
+__global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const BwdArgs a) {
   using E = Elt<T>;
   using Frag = typename E::Frag;
   constexpr int BN = kDqBN;
   constexpr int KK = D / 16, DB = D / 32;
-  constexpr int PITCH = D * (int)sizeof(T) + 16;
-  constexpr int TILE = BN * PITCH;
+  constexpr int TILE = LdsTile<T, D>::bytes(BN);
   __shared__ __attribute__((aligned(16))) char smem[2][2][TILE];  // [buffer][K, V]
 
   const int rank = blockIdx.x / a.h_q;
@@ -273,7 +277,7 @@ __global__ void __launch_bounds__(kDqThreads) dq_kernel(const BwdArgs a) {
   const bool suffix = td.kind == 1;
   const int rows_all = a.total_prefix + a.total_suffix;
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, wave = uniform(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hh = lane >> 5;
   const int wq0 = td.row0 + 32 * wave;
   const bool wave_active = wq0 < td.row1;
@@ -326,8 +330,8 @@ __global__ void __launch_bounds__(kDqThreads) dq_kernel(const BwdArgs a) {
 
   if (ntiles > 0) {
     issue(0);
-    ldk.store(smem[0][0], PITCH, tid);
-    ldv.store(smem[0][1], PITCH, tid);
+    ldk.store(smem[0][0], tid);
+    ldv.store(smem[0][1], tid);
   }
   __syncthreads();
 
@@ -338,7 +342,8 @@ __global__ void __launch_bounds__(kDqThreads) dq_kernel(const BwdArgs a) {
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
     bool skip, full;
-    if (segA && suffix) {
+    const bool cross = segA && suffix;  // response queries x prefix keys: no causal mask
+    if (cross) {
       skip = false;
       full = k0 + BN <= kend;
     } else {
@@ -350,45 +355,41 @@ __global__ void __launch_bounds__(kDqThreads) dq_kernel(const BwdArgs a) {
     if (wave_active && !skip) {
       const char* Kt = smem[buf][0];
       const char* Vt = smem[buf][1];
-      f32x16 s[2], dp[2];
+      // two blocks of 32 keys, one after the other
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        s[kb] = f32x16{};
-        dp[kb] = f32x16{};
-        const char* krow = Kt + (32 * kb + n) * PITCH + 8 * hh * (int)sizeof(T);
-        const char* vrow = Vt + (32 * kb + n) * PITCH + 8 * hh * (int)sizeof(T);
+        f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
-          s[kb] = E::mma(E::lds_row(krow + 16 * kk * (int)sizeof(T)), qf[kk], s[kb]);
-          dp[kb] = E::mma(E::lds_row(vrow + 16 * kk * (int)sizeof(T)), gf[kk], dp[kb]);
+          s = E::mma(E::template lds_row<D>(Kt, 32 * kb + n, 2 * kk + hh), qf[kk], s);
+          dp = E::mma(E::template lds_row<D>(Vt, 32 * kb + n, 2 * kk + hh), gf[kk], dp);
         }
-      }
+        auto softmax_grad = [&](auto masked) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float p = fast_exp2(s[kb][r] * c - lse2);
-          if (!full) {
-            const int kidx = k0 + 32 * kb + 8 * (r >> 2) + 4 * hh + (r & 3);
-            bool ok = kidx < kend;
-            if (!(segA && suffix)) ok = ok && kidx <= qrow_c;
-            if (!segA) ok = ok && kidx >= seg_q;
-            p = ok ? p : 0.f;
+          for (int r = 0; r < 16; ++r) {
+            float p = fast_exp2(fmaf(s[r], c, -lse2));
+            if (decltype(masked)::value) {
+              const int kidx = k0 + 32 * kb + 8 * (r >> 2) + 4 * hh + (r & 3);
+              const bool ok = (kidx < kend) & ((kidx <= qrow_c) | cross) & ((kidx >= seg_q) | segA);
+              p = ok ? p : 0.f;
+            }
+            dp[r] = p * (dp[r] - dsum);
           }
-          dp[kb][r] = p * (dp[kb][r] - dsum);
+        };
+        if (full) softmax_grad(std::false_type{}); else softmax_grad(std::true_type{});
+        // dQ^T += K^T dS^T over these 32 keys (two k steps of 16)
+#pragma unroll
+        for (int t2 = 0; t2 < 2; ++t2) {
+          const Frag dsf = E::acc_to_frag(dp, t2);
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+            acc[db] = E::mma(E::template lds_tr<D>(Kt, 16 * (2 * kb + t2), 32 * db, lane), dsf, acc[db]);
         }
-      }
-      // dQ^T += K^T dS^T (k = the 64 keys in 4 steps)
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const Frag dsf = E::acc_to_frag(dp[t >> 1], t & 1);
-#pragma unroll
-        for (int db = 0; db < DB; ++db) acc[db] = E::mma(E::lds_tr(Kt, PITCH, 16 * t, 32 * db, lane), dsf, acc[db]);
       }
     }
     if (j + 1 < ntiles) {
-      ldk.store(smem[buf ^ 1][0], PITCH, tid);
-      ldv.store(smem[buf ^ 1][1], PITCH, tid);
+      ldk.store(smem[buf ^ 1][0], tid);
+      ldv.store(smem[buf ^ 1][1], tid);
     }
     __syncthreads();
   }

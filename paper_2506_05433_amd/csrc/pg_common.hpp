@@ -46,9 +46,45 @@ struct GroupInfo {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
+// wave-uniform value held in a scalar register
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
 __device__ __forceinline__ float wave_swap32_max(float v) {
   return fmaxf(v, __shfl_xor(v, 32));
 }
+
+// ---------------------------------------------------------------- LDS tile addressing
+// A tile is `rows` rows of D elements, row-major. bf16 tiles use an unpadded pitch and
+// an XOR swizzle of their 16-byte chunks, chosen so that both access patterns of the
+// kernels are free of bank conflicts on the 64 x 4-byte LDS banks:
+//  * row-fragment reads (ds_read_b128): 16 lanes read one chunk of 16 consecutive rows;
+//  * transposing reads (ds_read_b64_tr_b16): 32 lanes read 4 consecutive chunks of
+//    4 consecutive rows (row index a multiple of 4 at the start).
+// For 16-chunk rows (D = 128) the chunk of row r is XORed with 4(r&3) + ((r>>2)&3); for
+// 8-chunk rows (D = 64, two rows per bank line) with 4((r>>1)&1) + ((r>>2)&3). Both maps
+// send 16 consecutive rows to distinct bank groups for a fixed chunk, and 4 rows x 4
+// chunks to distinct bank groups. fp32 tiles keep a 16-byte row pad instead.
+template <typename T, int D>
+struct LdsTile {
+  static constexpr int kRowBytes = D * (int)sizeof(T);
+  static constexpr int kChunks = kRowBytes / 16;
+  static constexpr bool kSwizzle = sizeof(T) == 2 && (kChunks == 16 || kChunks == 8);
+  static constexpr int kPitch = kSwizzle ? kRowBytes : kRowBytes + 16;
+  __device__ __forceinline__ static int swz(int row) {
+    if (!kSwizzle) return 0;
+    return kChunks == 16 ? (4 * (row & 3) + ((row >> 2) & 3)) : (4 * ((row >> 1) & 1) + ((row >> 2) & 3));
+  }
+  // byte offset of 16-byte chunk `chunk` of row `row`
+  __device__ __forceinline__ static int chunk_off(int row, int chunk) {
+    return row * kPitch + 16 * (chunk ^ swz(row));
+  }
+  // byte offset of element `col` of row `row` (any element inside a chunk)
+  __device__ __forceinline__ static int elem_off(int row, int col) {
+    const int b = col * (int)sizeof(T);
+    return chunk_off(row, b >> 4) + (b & 15);
+  }
+  static constexpr int bytes(int rows) { return rows * kPitch; }
+};
 
 // ---------------------------------------------------------------- element traits
 template <typename T>
@@ -61,17 +97,25 @@ struct Elt<bf16> {
   __device__ __forceinline__ static f32x16 mma(const Frag& a, const Frag& b, const f32x16& c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
-  // 8 consecutive elements at an LDS byte address (16-byte aligned)
-  __device__ __forceinline__ static Frag lds_row(const char* p) { return *(const Frag*)p; }
-  // transposed operand from a row-major LDS tile: element s of the result is
-  // tile[row(s)][col] with row(s) = r0 + s (s<4) or r0 + 8 + (s-4) (s>=4), where
-  // r0 = base_row + 4*h and col = base_col + l%32 (see the ds_read_tr16_b64 note).
-  __device__ __forceinline__ static Frag lds_tr(const char* tile, int pitch, int base_row, int base_col, int lane) {
+  // the 8 elements [8*half8, 8*half8+8) of row `row` (one 16-byte chunk)
+  template <int D>
+  __device__ __forceinline__ static Frag lds_row(const char* tile, int row, int chunk) {
+    return *(const Frag*)(tile + LdsTile<bf16, D>::chunk_off(row, chunk));
+  }
+  // Transposed operand from a row-major tile: element s of the result is
+  // tile[row(s)][col] with row(s) = base_row + 4h + (s & 3) + 8 (s >> 2) and
+  // col = base_col + l%32. ds_read_b64_tr_b16 works on groups of 16 lanes: lane i of
+  // a group receives element i%4 of the 8-byte rows addressed by lanes 4v + i/4,
+  // v = 0..3, so lane j of the group addresses row base_row + 4h + j/4 at column
+  // base_col + 16 g16 + 4 (j%4) and gets column base_col + 16 g16 + i of 4 rows.
+  template <int D>
+  __device__ __forceinline__ static Frag lds_tr(const char* tile, int base_row, int base_col, int lane) {
+    using L = LdsTile<bf16, D>;
     const int g16 = (lane & 31) >> 4, j = lane & 15, h = lane >> 5;
     const int row = base_row + 4 * h + (j >> 2);
     const int col = base_col + 16 * g16 + 4 * (j & 3);
-    const char* p0 = tile + row * pitch + col * 2;
-    const char* p1 = p0 + 8 * pitch;
+    const char* p0 = tile + L::elem_off(row, col);
+    const char* p1 = tile + L::elem_off(row + 8, col);
     i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p0));
     i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p1));
     // whole-vector shuffle + bit cast (element-wise bf16 inserts are lowered badly)
@@ -109,21 +153,25 @@ struct Elt<float> {
     for (int s = 0; s < 8; ++s) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a.v[s], b.v[s], c, 0, 0, 0);
     return c;
   }
-  __device__ __forceinline__ static Frag lds_row(const char* p) {
+  template <int D>
+  __device__ __forceinline__ static Frag lds_row(const char* tile, int row, int chunk) {
+    // `chunk` counts 8-element groups (32 bytes for fp32)
+    const char* p = tile + LdsTile<float, D>::elem_off(row, 8 * chunk);
     f32x4 a = *(const f32x4*)p, b = *(const f32x4*)(p + 16);
     Frag f;
     f.v[0] = a[0]; f.v[1] = a[1]; f.v[2] = a[2]; f.v[3] = a[3];
     f.v[4] = b[0]; f.v[5] = b[1]; f.v[6] = b[2]; f.v[7] = b[3];
     return f;
   }
-  __device__ __forceinline__ static Frag lds_tr(const char* tile, int pitch, int base_row, int base_col, int lane) {
+  template <int D>
+  __device__ __forceinline__ static Frag lds_tr(const char* tile, int base_row, int base_col, int lane) {
     const int h = lane >> 5;
     const int col = base_col + (lane & 31);
     Frag f;
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       const int row = base_row + 4 * h + (s & 3) + 8 * (s >> 2);
-      f.v[s] = *(const float*)(tile + row * pitch + col * 4);
+      f.v[s] = *(const float*)(tile + LdsTile<float, D>::elem_off(row, col));
     }
     return f;
   }
@@ -151,7 +199,7 @@ struct Elt<float> {
 };
 
 // Cooperative copy of `rows` rows of D elements (global row stride `gstride` elements)
-// into a row-major LDS tile with byte pitch `pitch`. Rows at or past `valid_rows` are
+// into an LDS tile laid out by LdsTile<T, D>. Rows at or past `valid_rows` are
 // zero-filled. Done in two phases (load to registers, store to LDS) so the caller can
 // overlap the global latency with compute.
 template <typename T, int ROWS, int D, int NT>
@@ -162,22 +210,23 @@ struct TileLoader {
   static_assert(kTotal % NT == 0, "tile must split evenly over the threads");
   uint4 reg[kPer];
   __device__ __forceinline__ void load(const T* base, int gstride, int valid_rows, int tid) {
+    // rows past the end are read from the last valid row and replaced by zeros (no branches)
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       const int c = tid + i * NT;
       const int r = c / kChunks, k = c % kChunks;
-      if (r < valid_rows)
-        reg[i] = *(const uint4*)((const char*)(base + (size_t)r * gstride) + 16 * k);
-      else
-        reg[i] = uint4{0u, 0u, 0u, 0u};
+      const int rc = r < valid_rows ? r : valid_rows - 1;
+      const uint4 v = *(const uint4*)((const char*)(base + (size_t)rc * gstride) + 16 * k);
+      const bool ok = r < valid_rows;
+      reg[i] = uint4{ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u};
     }
   }
-  __device__ __forceinline__ void store(char* lds, int pitch, int tid) const {
+  __device__ __forceinline__ void store(char* lds, int tid) const {
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       const int c = tid + i * NT;
       const int r = c / kChunks, k = c % kChunks;
-      *(uint4*)(lds + r * pitch + 16 * k) = reg[i];
+      *(uint4*)(lds + LdsTile<T, D>::chunk_off(r, k)) = reg[i];
     }
   }
 };

@@ -14,6 +14,8 @@
 // (l, l^32). P^T is then directly the B operand of O^T += V^T P^T; V^T comes from
 // the row-major LDS tile through transposing reads.
 #pragma once
+#include <type_traits>
+
 #include "pg_common.hpp"
 #include "pg_plan.hpp"
 
@@ -37,14 +39,16 @@ constexpr int kFwdBN = 64;   // keys per tile
 constexpr int kFwdThreads = 256;
 
 template <typename T, int D>
-__global__ void __launch_bounds__(kFwdThreads) fwd_kernel(const FwdArgs a) {
+#ifndef PG_FWD_MIN_BLOCKS
+#define PG_FWD_MIN_BLOCKS 2
+#endif
+__global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(const FwdArgs a) {
   using E = Elt<T>;
   using Frag = typename E::Frag;
   constexpr int BN = kFwdBN;
   constexpr int KK = D / 16;  // k steps over head_dim
   constexpr int DB = D / 32;  // 32-wide blocks of head_dim
-  constexpr int PITCH = D * (int)sizeof(T) + 16;
-  constexpr int TILE = BN * PITCH;
+  constexpr int TILE = LdsTile<T, D>::bytes(BN);
   __shared__ __attribute__((aligned(16))) char smem[2][2][TILE];  // [buffer][K, V]
 
   const int rank = blockIdx.x / a.h_q;
@@ -55,7 +59,7 @@ __global__ void __launch_bounds__(kFwdThreads) fwd_kernel(const FwdArgs a) {
   const int kvh = head / (a.h_q / a.h_kv);
   const bool suffix = td.kind == 1;
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, wave = uniform(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hh = lane >> 5;
   const int wq0 = td.row0 + 32 * wave;             // first row of this wave
   const bool wave_active = wq0 < td.row1;
@@ -105,8 +109,8 @@ __global__ void __launch_bounds__(kFwdThreads) fwd_kernel(const FwdArgs a) {
 
   if (ntiles > 0) {
     issue(0);
-    ldk.store(smem[0][0], PITCH, tid);
-    ldv.store(smem[0][1], PITCH, tid);
+    ldk.store(smem[0][0], tid);
+    ldv.store(smem[0][1], tid);
   }
   __syncthreads();
 
@@ -118,7 +122,8 @@ __global__ void __launch_bounds__(kFwdThreads) fwd_kernel(const FwdArgs a) {
     const int kend = segA ? kA1 : kB1;
     // visibility of this key tile to this wave
     bool skip, full;
-    if (segA && suffix) {
+    const bool cross = segA && suffix;  // response queries x prefix keys: no causal mask
+    if (cross) {
       skip = false;
       full = k0 + BN <= kend;
     } else {
@@ -135,28 +140,30 @@ __global__ void __launch_bounds__(kFwdThreads) fwd_kernel(const FwdArgs a) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         s[kb] = f32x16{};
-        const char* krow = Kt + (32 * kb + n) * PITCH + 8 * hh * (int)sizeof(T);
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) s[kb] = E::mma(E::lds_row(krow + 16 * kk * (int)sizeof(T)), qf[kk], s[kb]);
+        for (int kk = 0; kk < KK; ++kk)
+          s[kb] = E::mma(E::template lds_row<D>(Kt, 32 * kb + n, 2 * kk + hh), qf[kk], s[kb]);
       }
-      // scale, mask, tile max
+      // mask (only on tiles that straddle a boundary, branch-free) and tile max of the raw scores
       float tmax = -INFINITY;
+      auto mask_max = [&](auto masked) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+        for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float v = s[kb][r] * c;
-          if (!full) {
-            const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * hh + (r & 3);
-            bool ok = key < kend;
-            if (!(segA && suffix)) ok = ok && key <= qrow_c;
-            if (!segA) ok = ok && key >= seg_q;
-            v = ok ? v : -INFINITY;
+          for (int r = 0; r < 16; ++r) {
+            float v = s[kb][r];
+            if (decltype(masked)::value) {
+              const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * hh + (r & 3);
+              const bool ok = (key < kend) & ((key <= qrow_c) | cross) & ((key >= seg_q) | segA);
+              v = ok ? v : -INFINITY;
+            }
+            s[kb][r] = v;
+            tmax = fmaxf(tmax, v);
           }
-          s[kb][r] = v;
-          tmax = fmaxf(tmax, v);
         }
-      }
+      };
+      if (full) mask_max(std::false_type{}); else mask_max(std::true_type{});
+      tmax *= c;  // c > 0: max(c*s) = c*max(s)
       tmax = wave_swap32_max(tmax);
       const float m_new = fmaxf(m_run, tmax);
       const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
@@ -166,7 +173,7 @@ __global__ void __launch_bounds__(kFwdThreads) fwd_kernel(const FwdArgs a) {
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(s[kb][r] - m_use);
+          const float p = fast_exp2(fmaf(s[kb][r], c, -m_use));
           s[kb][r] = p;
           psum += p;
         }
@@ -181,14 +188,14 @@ __global__ void __launch_bounds__(kFwdThreads) fwd_kernel(const FwdArgs a) {
         const Frag pf = E::acc_to_frag(s[t >> 1], t & 1);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const Frag vf = E::lds_tr(Vt, PITCH, 16 * t, 32 * db, lane);
+          const Frag vf = E::template lds_tr<D>(Vt, 16 * t, 32 * db, lane);
           acc_o[db] = E::mma(vf, pf, acc_o[db]);
         }
       }
     }
     if (j + 1 < ntiles) {
-      ldk.store(smem[buf ^ 1][0], PITCH, tid);
-      ldv.store(smem[buf ^ 1][1], PITCH, tid);
+      ldk.store(smem[buf ^ 1][0], tid);
+      ldv.store(smem[buf ^ 1][1], tid);
     }
     __syncthreads();
   }
