@@ -191,7 +191,7 @@ int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p,
 
 template <typename T, int D>
 void launch_fwd(const pg::FwdArgs& a, long max_q, hipStream_t st) {
-  const long blocks = max_q * a.h_q;
+  const long blocks = pg::xcd_grid_blocks(max_q, a.h_q, a.h_q / a.h_kv);
   Timed tm(PG_K_FWD, st);
   if (blocks > 0) hipLaunchKernelGGL((pg::fwd_kernel<T, D>), dim3((unsigned)blocks), dim3(pg::kFwdThreads), 0, st, a);
 }
@@ -206,11 +206,13 @@ void launch_bwd(const pg::BwdArgs& a, long max_q, long max_kv, hipStream_t st) {
   }
   if (max_kv > 0) {
     Timed tm(PG_K_DKDV, st);
-    hipLaunchKernelGGL((pg::dkdv_kernel<T, D>), dim3((unsigned)(max_kv * a.h_kv)), dim3(pg::kKvThreads), 0, st, a);
+    const long blocks = pg::xcd_grid_blocks(max_kv, a.h_kv, 1);
+    hipLaunchKernelGGL((pg::dkdv_kernel<T, D>), dim3((unsigned)blocks), dim3(pg::kKvThreads), 0, st, a);
   }
   if (max_q > 0) {
     Timed tm(PG_K_DQ, st);
-    hipLaunchKernelGGL((pg::dq_kernel<T, D>), dim3((unsigned)(max_q * a.h_q)), dim3(pg::kDqThreads), 0, st, a);
+    const long blocks = pg::xcd_grid_blocks(max_q, a.h_q, a.h_q / a.h_kv);
+    hipLaunchKernelGGL((pg::dq_kernel<T, D>), dim3((unsigned)blocks), dim3(pg::kDqThreads), 0, st, a);
   }
 }
 

@@ -16,8 +16,6 @@
 //         from the accumulators as B operands and dO^T, Q^T through transposing LDS reads.
 //   dq  : S^T = K Q^T and dP^T = V dO^T with queries as columns; dQ^T += K^T dS^T.
 #pragma once
-#include <type_traits>
-
 #include "pg_common.hpp"
 #include "pg_plan.hpp"
 
@@ -77,8 +75,8 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
   __shared__ __attribute__((aligned(16))) float s_dsum[2][BQ];
   __shared__ int s_seg[2][BQ];
 
-  const int rank = blockIdx.x / a.h_kv;
-  const int kvh = blockIdx.x % a.h_kv;
+  const BlockSlot slot = xcd_slot(blockIdx.x, a.h_kv, 1);
+  const int rank = slot.unit, kvh = slot.head;
   if (rank >= a.hdr->n_kvtiles) return;
   const TileDesc td = a.kvtiles[a.kvorder[rank]];
   const GroupInfoEx gi = a.ginfo[td.group];
@@ -195,30 +193,36 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
         // P = exp2(S*c - lse*log2e) (0 on padding rows, whose lse is +inf);
         // dS = P * (dP - Dsum); rows are queries, the lane's column is its key.
         // The mask is only evaluated on tiles that straddle a boundary, branch-free.
-        auto softmax_grad = [&](auto masked) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const f32x4 l4 = *(const f32x4*)&s_lse[buf][32 * qb + 8 * i + 4 * hh];
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) s[4 * i + jj] = fast_exp2(fmaf(s[4 * i + jj], c, -l4[jj]));
+        }
+        if (!full) {
+          // boundary tile: query offset o = 8i + jj of register r = 4i + jj sees the lane's
+          // key iff o >= lim (causal) and the key is not before the query's member start
+          asm volatile("");
+          const int lim = key_c - (q0 + 32 * qb + 4 * hh);
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const int qi = 32 * qb + 8 * i + 4 * hh;
-            const f32x4 l4 = *(const f32x4*)&s_lse[buf][qi];
-            const f32x4 d4 = *(const f32x4*)&s_dsum[buf][qi];
             int4 g4 = int4{0, 0, 0, 0};
-            if (decltype(masked)::value) g4 = *(const int4*)&s_seg[buf][qi];
+            if (kv_suffix) g4 = *(const int4*)&s_seg[buf][32 * qb + 8 * i + 4 * hh];
             const int gs[4] = {g4.x, g4.y, g4.z, g4.w};
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
-              const int r = 4 * i + jj;
-              float p = fast_exp2(fmaf(s[r], c, -l4[jj]));
-              if (decltype(masked)::value) {
-                const int q = q0 + qi + jj;
-                const bool ok = (key_c <= q) & (key_c >= gs[jj]);
-                p = ok ? p : 0.f;
-              }
-              s[r] = p;
-              dp[r] = p * (dp[r] - d4[jj]);
+              const int o = 8 * i + jj;
+              const bool ok = (o >= lim) & (key_c >= gs[jj]);
+              s[4 * i + jj] = ok ? s[4 * i + jj] : 0.f;
             }
           }
-        };
-        if (full) softmax_grad(std::false_type{}); else softmax_grad(std::true_type{});
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const f32x4 d4 = *(const f32x4*)&s_dsum[buf][32 * qb + 8 * i + 4 * hh];
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) dp[4 * i + jj] = s[4 * i + jj] * (dp[4 * i + jj] - d4[jj]);
+        }
         // dV^T += dO^T P ; dK^T += Q^T dS over these 32 queries (two k steps of 16)
 #pragma unroll
         for (int t2 = 0; t2 < 2; ++t2) {
@@ -268,8 +272,8 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
   constexpr int TILE = LdsTile<T, D>::bytes(BN);
   __shared__ __attribute__((aligned(16))) char smem[2][2][TILE];  // [buffer][K, V]
 
-  const int rank = blockIdx.x / a.h_q;
-  const int head = blockIdx.x % a.h_q;
+  const BlockSlot slot = xcd_slot(blockIdx.x, a.h_q, a.h_q / a.h_kv);
+  const int rank = slot.unit, head = slot.head;
   if (rank >= a.hdr->n_qtiles) return;
   const TileDesc td = a.qtiles[a.qorder[rank]];
   const GroupInfoEx gi = a.ginfo[td.group];
@@ -364,19 +368,24 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
           s = E::mma(E::template lds_row<D>(Kt, 32 * kb + n, 2 * kk + hh), qf[kk], s);
           dp = E::mma(E::template lds_row<D>(Vt, 32 * kb + n, 2 * kk + hh), gf[kk], dp);
         }
-        auto softmax_grad = [&](auto masked) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          s[r] = fast_exp2(fmaf(s[r], c, -lse2));
+        }
+        if (!full) {  // boundary tile: zero the invisible keys (see the forward kernel)
+          asm volatile("");
+          const int base = k0 + 32 * kb + 4 * hh;
+          int hi = kend - base;
+          if (!cross) hi = min(hi, qrow_c + 1 - base);
+          const int lo = segA ? -(1 << 30) : seg_q - base;
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            float p = fast_exp2(fmaf(s[r], c, -lse2));
-            if (decltype(masked)::value) {
-              const int kidx = k0 + 32 * kb + 8 * (r >> 2) + 4 * hh + (r & 3);
-              const bool ok = (kidx < kend) & ((kidx <= qrow_c) | cross) & ((kidx >= seg_q) | segA);
-              p = ok ? p : 0.f;
-            }
-            dp[r] = p * (dp[r] - dsum);
+            const int o = 8 * (r >> 2) + (r & 3);
+            s[r] = ((o >= lo) & (o < hi)) ? s[r] : 0.f;
           }
-        };
-        if (full) softmax_grad(std::false_type{}); else softmax_grad(std::true_type{});
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dp[r] = s[r] * (dp[r] - dsum);
         // dQ^T += K^T dS^T over these 32 keys (two k steps of 16)
 #pragma unroll
         for (int t2 = 0; t2 < 2; ++t2) {

@@ -14,8 +14,6 @@
 // (l, l^32). P^T is then directly the B operand of O^T += V^T P^T; V^T comes from
 // the row-major LDS tile through transposing reads.
 #pragma once
-#include <type_traits>
-
 #include "pg_common.hpp"
 #include "pg_plan.hpp"
 
@@ -51,8 +49,8 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
   constexpr int TILE = LdsTile<T, D>::bytes(BN);
   __shared__ __attribute__((aligned(16))) char smem[2][2][TILE];  // [buffer][K, V]
 
-  const int rank = blockIdx.x / a.h_q;
-  const int head = blockIdx.x % a.h_q;
+  const BlockSlot slot = xcd_slot(blockIdx.x, a.h_q, a.h_q / a.h_kv);
+  const int rank = slot.unit, head = slot.head;
   if (rank >= a.hdr->n_qtiles) return;
   const TileDesc td = a.qtiles[a.qorder[rank]];
   const GroupInfoEx gi = a.ginfo[td.group];
@@ -144,30 +142,35 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
         for (int kk = 0; kk < KK; ++kk)
           s[kb] = E::mma(E::template lds_row<D>(Kt, 32 * kb + n, 2 * kk + hh), qf[kk], s[kb]);
       }
-      // mask (only on tiles that straddle a boundary, branch-free) and tile max of the raw scores
-      float tmax = -INFINITY;
-      auto mask_max = [&](auto masked) {
+      // Mask, only on tiles that straddle a boundary (a real branch: the empty asm keeps
+      // the compiler from turning it into selects executed on every tile). Key offset
+      // o = 32kb + 8(r/4) + r%4 of register r is a compile-time constant; the lane's
+      // visible offsets are [lo, hi).
+      if (!full) {
+        asm volatile("");
+        const int base = k0 + 4 * hh;
+        int hi = kend - base;
+        if (!cross) hi = min(hi, qrow_c + 1 - base);
+        const int lo = segA ? -(1 << 30) : seg_q - base;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            float v = s[kb][r];
-            if (decltype(masked)::value) {
-              const int key = k0 + 32 * kb + 8 * (r >> 2) + 4 * hh + (r & 3);
-              const bool ok = (key < kend) & ((key <= qrow_c) | cross) & ((key >= seg_q) | segA);
-              v = ok ? v : -INFINITY;
-            }
-            s[kb][r] = v;
-            tmax = fmaxf(tmax, v);
+            const int o = 32 * kb + 8 * (r >> 2) + (r & 3);
+            s[kb][r] = ((o >= lo) & (o < hi)) ? s[kb][r] : -INFINITY;
           }
-        }
-      };
-      if (full) mask_max(std::false_type{}); else mask_max(std::true_type{});
-      tmax *= c;  // c > 0: max(c*s) = c*max(s)
-      tmax = wave_swap32_max(tmax);
-      const float m_new = fmaxf(m_run, tmax);
+      }
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
+      tmax = wave_swap32_max(tmax) * c;  // c > 0: max(c*s) = c*max(s)
+      // Lazy running max: a row keeps its max until a tile exceeds it by more than
+      // 2^8, so most tiles need no rescale of O (p <= 256 is harmless in fp32/bf16;
+      // the log-sum-exp is exact for any choice of m).
+      const float m_new = (tmax > m_run + 8.f) ? tmax : m_run;
       const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = fast_exp2(m_run - m_use);
       float psum = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
@@ -178,10 +181,14 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
           psum += p;
         }
       }
-      l_run = l_run * alpha + psum;
-      m_run = m_new;
+      if (__any(m_new != m_run)) {
+        const float alpha = fast_exp2(m_run - m_use);
+        l_run *= alpha;
 #pragma unroll
-      for (int db = 0; db < DB; ++db) acc_o[db] *= alpha;
+        for (int db = 0; db < DB; ++db) acc_o[db] *= alpha;
+      }
+      l_run += psum;
+      m_run = m_new;
       // O^T += V^T P^T over the 64 keys (4 k steps of 16)
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
