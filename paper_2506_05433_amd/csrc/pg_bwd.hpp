@@ -59,21 +59,38 @@ __global__ void __launch_bounds__(256) bwd_dot_kernel(const BwdArgs a) {
 }
 
 // ------------------------------------------------------------------ dK, dV (key-stationary)
-constexpr int kKvBN = 128;  // keys per workgroup (32 per wave)
-constexpr int kKvBQ = 64;   // query rows per staged tile
-constexpr int kKvThreads = 256;
+// A workgroup owns 128 keys of one kv head, split into four groups of 32. Each key
+// group is served by two waves that share a SIMD:
+//   P-wave : S = Q K^T, P = exp(S*scale - lse) (masked), dV^T += dO^T P; it hands P
+//            (bf16 operand fragments) to its partner through LDS;
+//   G-wave : one query tile behind, dP = dO V^T, dS = P (dP - Dsum), dK^T += Q^T dS.
+// Each wave therefore holds one kv operand and one accumulator (about half the
+// registers of a wave doing all four products), so two waves fit per SIMD and one's
+// exp/VALU work overlaps the other's matrix instructions. Query tiles are
+// triple-buffered in LDS (P-waves read tile i, G-waves tile i-1, tile i+1 loads).
+constexpr int kKvBN = 128;  // keys per workgroup
+constexpr int kKvThreads = 512;
+
+template <typename T>
+struct KvTileRows {
+  static constexpr int value = sizeof(T) == 2 ? 64 : 32;
+};
 
 template <typename T, int D>
 __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
   using E = Elt<T>;
   using Frag = typename E::Frag;
-  constexpr int BQ = kKvBQ;
+  constexpr int BQ = KvTileRows<T>::value;  // query rows per staged tile
+  constexpr int QB = BQ / 32;               // 32-row halves
+  constexpr int NT = BQ / 16;               // 16-wide k steps over the tile's queries
   constexpr int KK = D / 16, DB = D / 32;
+  constexpr int NBUF = 3;
   constexpr int TILE = LdsTile<T, D>::bytes(BQ);
-  __shared__ __attribute__((aligned(16))) char smem[2][2][TILE];  // [buffer][Q, dO]
-  __shared__ __attribute__((aligned(16))) float s_lse[2][BQ];     // lse * log2(e), +inf for padding
-  __shared__ __attribute__((aligned(16))) float s_dsum[2][BQ];
-  __shared__ int s_seg[2][BQ];
+  __shared__ __attribute__((aligned(16))) char smem[NBUF][2][TILE];  // [buffer][Q, dO]
+  __shared__ __attribute__((aligned(16))) float s_lse[NBUF][BQ];     // lse * log2(e), +inf for padding
+  __shared__ __attribute__((aligned(16))) float s_dsum[NBUF][BQ];
+  __shared__ __attribute__((aligned(16))) int s_seg[NBUF][BQ];
+  __shared__ __attribute__((aligned(16))) Frag s_p[2][4][NT][64];  // P handoff [buffer][key group][k step][lane]
 
   const BlockSlot slot = xcd_slot(blockIdx.x, a.h_kv, 1);
   const int rank = slot.unit, kvh = slot.head;
@@ -86,27 +103,26 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
 
   const int tid = threadIdx.x, wave = uniform(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hh = lane >> 5;
-  const int wk0 = td.row0 + 32 * wave;            // first key of this wave
+  const int grp = wave & 3;
+  const bool pwave = wave < 4;
+  const int wk0 = td.row0 + 32 * grp;             // first key of this key group
   const bool wave_active = wk0 < td.row1;
-  const int wk1 = min(wk0 + 32, td.row1) - 1;     // last valid key of this wave
+  const int wk1 = min(wk0 + 32, td.row1) - 1;     // last valid key of the group
   const int key = wk0 + n;
   const bool kvalid = key < td.row1;
   const int key_c = kvalid ? key : td.row1 - 1;
 
-  const T* Kb = (const T*)(kv_suffix ? a.k_suf : a.k_pre);
-  const T* Vb = (const T*)(kv_suffix ? a.v_suf : a.v_pre);
-  Frag kf[KK], vf[KK];
+  // P-waves keep K, G-waves keep V (the B operand of their first product)
+  Frag kv[KK];
   {
+    const T* B = (const T*)(pwave ? (kv_suffix ? a.k_suf : a.k_pre) : (kv_suffix ? a.v_suf : a.v_pre));
     const size_t off = ((size_t)key_c * a.h_kv + kvh) * D + 8 * hh;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      kf[kk] = E::global_row(Kb + off + 16 * kk, kvalid);
-      vf[kk] = E::global_row(Vb + off + 16 * kk, kvalid);
-    }
+    for (int kk = 0; kk < KK; ++kk) kv[kk] = E::global_row(B + off + 16 * kk, kvalid);
   }
-  f32x16 dk[DB], dv[DB];
+  f32x16 acc[DB];  // dV^T (P-wave) or dK^T (G-wave)
 #pragma unroll
-  for (int db = 0; db < DB; ++db) { dk[db] = f32x16{}; dv[db] = f32x16{}; }
+  for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
 
   // Query ranges that see these keys, in fixed order:
   //   prefix keys  : prefix rows [row0, p1) (causal), then response rows [s0, s1) (dense)
@@ -121,30 +137,54 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
   const int total = per_head * ratio;
   const float c = a.scale_log2;
 
+  struct TileInfo {
+    int hq, q0, qend;
+    bool qsuf, causal;
+  };
+  auto info = [&](int it) {
+    TileInfo ti;
+    ti.hq = kvh * ratio + it / per_head;
+    const int j = it % per_head;
+    const bool first = j < n1;
+    ti.qsuf = first ? kv_suffix : true;
+    ti.q0 = first ? r1_lo + j * BQ : r2_lo + (j - n1) * BQ;
+    ti.qend = first ? r1_hi : r2_hi;
+    ti.causal = first;  // prefix keys x prefix rows, or response keys x response rows
+    return ti;
+  };
+  // visibility of a tile to this key group: skip (no pair visible) / full (all visible)
+  auto visibility = [&](const TileInfo& ti, int buf, bool& skip, bool& full) {
+    skip = false;
+    full = true;  // padding rows need no mask: their lse is +inf
+    if (ti.causal) {
+      skip = ti.q0 + BQ - 1 < wk0;                   // every query precedes every key
+      full = ti.q0 >= wk1;                            // every query sees every key
+      if (kv_suffix) {
+        const int last = min(ti.q0 + BQ, ti.qend) - 1 - ti.q0;
+        skip = skip || (s_seg[buf][0] > wk1);         // queries all belong to later members
+        full = full && (s_seg[buf][last] <= wk0);
+      }
+    }
+  };
+
   TileLoader<T, BQ, D, kKvThreads> ldq, ldo;
   float pf_lse = 0.f, pf_dsum = 0.f;
   int pf_seg = 0;
   auto issue = [&](int it) {
-    const int hq = kvh * ratio + it / per_head;
-    const int j = it % per_head;
-    const bool first = j < n1;
-    // first range: prefix rows for prefix keys, response rows for response keys
-    const bool qsuf = first ? kv_suffix : true;
-    const int q0 = first ? r1_lo + j * BQ : r2_lo + (j - n1) * BQ;
-    const int qend = first ? r1_hi : r2_hi;
-    const T* Qs = (const T*)(qsuf ? a.q_suf : a.q_pre);
-    const T* Gs = (const T*)(qsuf ? a.do_suf : a.do_pre);
-    const size_t off = ((size_t)q0 * a.h_q + hq) * D;
-    ldq.load(Qs + off, a.h_q * D, qend - q0, tid);
-    ldo.load(Gs + off, a.h_q * D, qend - q0, tid);
+    const TileInfo ti = info(it);
+    const T* Qs = (const T*)(ti.qsuf ? a.q_suf : a.q_pre);
+    const T* Gs = (const T*)(ti.qsuf ? a.do_suf : a.do_pre);
+    const size_t off = ((size_t)ti.q0 * a.h_q + ti.hq) * D;
+    ldq.load(Qs + off, a.h_q * D, ti.qend - ti.q0, tid);
+    ldo.load(Gs + off, a.h_q * D, ti.qend - ti.q0, tid);
     if (tid < BQ) {
-      const int q = q0 + tid;
-      const bool v = q < qend;
-      const float* L = qsuf ? a.lse_suf : a.lse_pre;
-      const int tot = qsuf ? a.total_suffix : a.total_prefix;
-      pf_lse = v ? L[(size_t)hq * tot + q] * kLog2e : INFINITY;
-      pf_dsum = v ? a.dsum[(size_t)hq * rows_all + (qsuf ? a.total_prefix : 0) + q] : 0.f;
-      pf_seg = (v && qsuf) ? a.seg_start[q] : 0;
+      const int q = ti.q0 + tid;
+      const bool v = q < ti.qend;
+      const float* L = ti.qsuf ? a.lse_suf : a.lse_pre;
+      const int tot = ti.qsuf ? a.total_suffix : a.total_prefix;
+      pf_lse = v ? L[(size_t)ti.hq * tot + q] * kLog2e : INFINITY;
+      pf_dsum = v ? a.dsum[(size_t)ti.hq * rows_all + (ti.qsuf ? a.total_prefix : 0) + q] : 0.f;
+      pf_seg = (v && ti.qsuf) ? a.seg_start[q] : 0;
     }
   };
   auto commit = [&](int buf) {
@@ -156,102 +196,107 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
   if (total > 0) { issue(0); commit(0); }
   __syncthreads();
 
-  for (int it = 0; it < total; ++it) {
-    const int buf = it & 1;
+  for (int it = 0; it <= total; ++it) {
     if (it + 1 < total) issue(it + 1);
-    const int j = it % per_head;
-    const bool first = j < n1;
-    const bool qsuf = first ? kv_suffix : true;
-    const int q0 = first ? r1_lo + j * BQ : r2_lo + (j - n1) * BQ;
-    const int qend = first ? r1_hi : r2_hi;
-    // masking mode: causal when queries and keys are on the same side
-    const bool causal = first;  // prefix keys x prefix rows, or response keys x response rows
-    bool skip = false, full = true;  // padding rows need no mask: their lse is +inf
-    if (causal) {
-      skip = q0 + BQ - 1 < wk0;                      // every query precedes every key
-      full = full && (q0 >= wk1);                    // every query sees every key
-      if (kv_suffix) {
-        const int seg_lo = s_seg[buf][0];
-        const int last = min(q0 + BQ, qend) - 1 - q0;
-        const int seg_hi = s_seg[buf][last];
-        skip = skip || (seg_lo > wk1);               // queries all belong to later members
-        full = full && (seg_hi <= wk0);
-      }
-    }
-    if (wave_active && !skip) {
-      const char* Qt = smem[buf][0];
-      const char* Gt = smem[buf][1];
-      // two halves of 32 query rows, one after the other (keeps S and dP of 32 rows live)
+    if (pwave && it < total && wave_active) {
+      // ---------------- P-wave on tile it
+      const int buf = it % NBUF;
+      const TileInfo ti = info(it);
+      bool skip, full;
+      visibility(ti, buf, skip, full);
+      if (!skip) {
+        const char* Qt = smem[buf][0];
+        const char* Gt = smem[buf][1];
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        f32x16 s = f32x16{}, dp = f32x16{};
+        for (int qb = 0; qb < QB; ++qb) {
+          f32x16 sc = f32x16{};
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          s = E::mma(E::template lds_row<D>(Qt, 32 * qb + n, 2 * kk + hh), kf[kk], s);
-          dp = E::mma(E::template lds_row<D>(Gt, 32 * qb + n, 2 * kk + hh), vf[kk], dp);
-        }
-        // P = exp2(S*c - lse*log2e) (0 on padding rows, whose lse is +inf);
-        // dS = P * (dP - Dsum); rows are queries, the lane's column is its key.
-        // The mask is only evaluated on tiles that straddle a boundary, branch-free.
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const f32x4 l4 = *(const f32x4*)&s_lse[buf][32 * qb + 8 * i + 4 * hh];
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) s[4 * i + jj] = fast_exp2(fmaf(s[4 * i + jj], c, -l4[jj]));
-        }
-        if (!full) {
-          // boundary tile: query offset o = 8i + jj of register r = 4i + jj sees the lane's
-          // key iff o >= lim (causal) and the key is not before the query's member start
-          asm volatile("");
-          const int lim = key_c - (q0 + 32 * qb + 4 * hh);
+          for (int kk = 0; kk < KK; ++kk)
+            sc = E::mma(E::template lds_row<D>(Qt, 32 * qb + n, 2 * kk + hh), kv[kk], sc);
+          // P = exp2(S*c - lse*log2e); rows are queries, the lane's column is its key
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            int4 g4 = int4{0, 0, 0, 0};
-            if (kv_suffix) g4 = *(const int4*)&s_seg[buf][32 * qb + 8 * i + 4 * hh];
-            const int gs[4] = {g4.x, g4.y, g4.z, g4.w};
+            const f32x4 l4 = *(const f32x4*)&s_lse[buf][32 * qb + 8 * i + 4 * hh];
 #pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-              const int o = 8 * i + jj;
-              const bool ok = (o >= lim) & (key_c >= gs[jj]);
-              s[4 * i + jj] = ok ? s[4 * i + jj] : 0.f;
+            for (int jj = 0; jj < 4; ++jj) sc[4 * i + jj] = fast_exp2(fmaf(sc[4 * i + jj], c, -l4[jj]));
+          }
+          if (!full) {
+            // boundary tile: query offset o = 8i + jj of register r = 4i + jj sees the lane's
+            // key iff o >= lim (causal) and the key is not before the query's member start
+            asm volatile("");
+            const int lim = key_c - (ti.q0 + 32 * qb + 4 * hh);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              int4 g4 = int4{0, 0, 0, 0};
+              if (kv_suffix) g4 = *(const int4*)&s_seg[buf][32 * qb + 8 * i + 4 * hh];
+              const int gs[4] = {g4.x, g4.y, g4.z, g4.w};
+#pragma unroll
+              for (int jj = 0; jj < 4; ++jj) {
+                const int o = 8 * i + jj;
+                const bool ok = (o >= lim) & (key_c >= gs[jj]);
+                sc[4 * i + jj] = ok ? sc[4 * i + jj] : 0.f;
+              }
             }
           }
+          // hand P to the G-wave and accumulate dV^T += dO^T P over these 32 queries
+#pragma unroll
+          for (int t2 = 0; t2 < 2; ++t2) {
+            const int t = 2 * qb + t2;
+            const Frag pf = E::acc_to_frag(sc, t2);
+            s_p[it & 1][grp][t][lane] = pf;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) acc[db] = E::mma(E::template lds_tr<D>(Gt, 16 * t, 32 * db, lane), pf, acc[db]);
+          }
         }
+      }
+    } else if (!pwave && it > 0 && wave_active) {
+      // ---------------- G-wave on tile it-1
+      const int buf = (it - 1) % NBUF;
+      const TileInfo ti = info(it - 1);
+      bool skip, full;
+      visibility(ti, buf, skip, full);
+      if (!skip) {
+        const char* Qt = smem[buf][0];
+        const char* Gt = smem[buf][1];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const f32x4 d4 = *(const f32x4*)&s_dsum[buf][32 * qb + 8 * i + 4 * hh];
+        for (int qb = 0; qb < QB; ++qb) {
+          f32x16 dp = f32x16{};
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) dp[4 * i + jj] = s[4 * i + jj] * (dp[4 * i + jj] - d4[jj]);
-        }
-        // dV^T += dO^T P ; dK^T += Q^T dS over these 32 queries (two k steps of 16)
+          for (int kk = 0; kk < KK; ++kk)
+            dp = E::mma(E::template lds_row<D>(Gt, 32 * qb + n, 2 * kk + hh), kv[kk], dp);
 #pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2) {
-          const int t = 2 * qb + t2;
-          const Frag pfr = E::acc_to_frag(s, t2);
-          const Frag dsf = E::acc_to_frag(dp, t2);
+          for (int t2 = 0; t2 < 2; ++t2) {
+            const int t = 2 * qb + t2;
+            const Frag pf = s_p[(it - 1) & 1][grp][t][lane];
+            f32x16 ds;  // only registers [8 t2, 8 t2 + 8) are used
 #pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            dv[db] = E::mma(E::template lds_tr<D>(Gt, 16 * t, 32 * db, lane), pfr, dv[db]);
-            dk[db] = E::mma(E::template lds_tr<D>(Qt, 16 * t, 32 * db, lane), dsf, dk[db]);
+            for (int e = 0; e < 8; ++e) {
+              const int r = 8 * t2 + e;
+              const float d = s_dsum[buf][32 * qb + 8 * (r >> 2) + 4 * hh + (r & 3)];
+              ds[r] = E::frag_elem(pf, e) * (dp[r] - d);
+            }
+            const Frag dsf = E::acc_to_frag(ds, t2);
+#pragma unroll
+            for (int db = 0; db < DB; ++db) acc[db] = E::mma(E::template lds_tr<D>(Qt, 16 * t, 32 * db, lane), dsf, acc[db]);
           }
         }
       }
     }
-    if (it + 1 < total) commit(buf ^ 1);
+    if (it + 1 < total) commit((it + 1) % NBUF);
     __syncthreads();
   }
 
   if (!wave_active || !kvalid) return;
-  T* dK = (T*)(kv_suffix ? a.dk_suf : a.dk_pre) + ((size_t)key * a.h_kv + kvh) * D;
-  T* dV = (T*)(kv_suffix ? a.dv_suf : a.dv_pre) + ((size_t)key * a.h_kv + kvh) * D;
-  const float sc = a.scale;
+  T* out = (T*)(pwave ? (kv_suffix ? a.dv_suf : a.dv_pre) : (kv_suffix ? a.dk_suf : a.dk_pre)) +
+           ((size_t)key * a.h_kv + kvh) * D;
+  const float sc = pwave ? 1.f : a.scale;
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int d0 = 32 * db + 8 * i + 4 * hh;
-      E::store4(dK + d0, dk[db][4 * i] * sc, dk[db][4 * i + 1] * sc, dk[db][4 * i + 2] * sc, dk[db][4 * i + 3] * sc);
-      E::store4(dV + d0, dv[db][4 * i], dv[db][4 * i + 1], dv[db][4 * i + 2], dv[db][4 * i + 3]);
+      E::store4(out + d0, acc[db][4 * i] * sc, acc[db][4 * i + 1] * sc, acc[db][4 * i + 2] * sc,
+                acc[db][4 * i + 3] * sc);
     }
 }
 

@@ -146,6 +146,12 @@ struct Elt<bf16> {
   __device__ __forceinline__ static f32x16 mma(const Frag& a, const Frag& b, const f32x16& c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
+  // Same product with the accumulator pinned to AGPRs. Long-lived accumulators of
+  // kernels that run one wave per SIMD stay in the accumulator file this way instead
+  // of being copied between register files around every instruction.
+  __device__ __forceinline__ static void mma_acc(f32x16& c, const Frag& a, const Frag& b) {
+    asm("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+  }
   // the 8 elements [8*half8, 8*half8+8) of row `row` (one 16-byte chunk)
   template <int D>
   __device__ __forceinline__ static Frag lds_row(const char* tile, int row, int chunk) {
@@ -185,6 +191,7 @@ struct Elt<bf16> {
     for (int s = 0; s < 8; ++s) f[s] = (bf16)acc[8 * half + s];
     return f;
   }
+  __device__ __forceinline__ static float frag_elem(const Frag& f, int e) { return (float)f[e]; }
   __device__ __forceinline__ static void store4(bf16* p, float a, float b, float c, float d) {
     bf16x4 v = {(bf16)a, (bf16)b, (bf16)c, (bf16)d};
     *(bf16x4*)p = v;
@@ -202,6 +209,7 @@ struct Elt<float> {
     for (int s = 0; s < 8; ++s) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a.v[s], b.v[s], c, 0, 0, 0);
     return c;
   }
+  __device__ __forceinline__ static void mma_acc(f32x16& c, const Frag& a, const Frag& b) { c = mma(a, b, c); }
   template <int D>
   __device__ __forceinline__ static Frag lds_row(const char* tile, int row, int chunk) {
     // `chunk` counts 8-element groups (32 bytes for fp32)
@@ -242,6 +250,7 @@ struct Elt<float> {
     for (int s = 0; s < 8; ++s) f.v[s] = acc[8 * half + s];
     return f;
   }
+  __device__ __forceinline__ static float frag_elem(const Frag& f, int e) { return f.v[e]; }
   __device__ __forceinline__ static void store4(float* p, float a, float b, float c, float d) {
     *(f32x4*)p = f32x4{a, b, c, d};
   }
