@@ -68,16 +68,23 @@ __global__ void __launch_bounds__(256) bwd_dot_kernel(const BwdArgs a) {
 // registers of a wave doing all four products), so two waves fit per SIMD and one's
 // exp/VALU work overlaps the other's matrix instructions. Query tiles are
 // triple-buffered in LDS (P-waves read tile i, G-waves tile i-1, tile i+1 loads).
-constexpr int kKvBN = 128;  // keys per workgroup
-constexpr int kKvThreads = 512;
+#ifndef PG_KV_GROUPS
+#define PG_KV_GROUPS 4
+#endif
+constexpr int kKvGroups = PG_KV_GROUPS;      // 32-key groups per workgroup
+constexpr int kKvBN = 32 * kKvGroups;        // keys per workgroup
+constexpr int kKvThreads = 128 * kKvGroups;  // a P-wave and a G-wave per key group
 
+#ifndef PG_KV_BQ_BF16
+#define PG_KV_BQ_BF16 64
+#endif
 template <typename T>
 struct KvTileRows {
-  static constexpr int value = sizeof(T) == 2 ? 64 : 32;
+  static constexpr int value = sizeof(T) == 2 ? PG_KV_BQ_BF16 : 32;
 };
 
 template <typename T, int D>
-__global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
+__global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(const BwdArgs a) {
   using E = Elt<T>;
   using Frag = typename E::Frag;
   constexpr int BQ = KvTileRows<T>::value;  // query rows per staged tile
@@ -90,7 +97,7 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
   __shared__ __attribute__((aligned(16))) float s_lse[NBUF][BQ];     // lse * log2(e), +inf for padding
   __shared__ __attribute__((aligned(16))) float s_dsum[NBUF][BQ];
   __shared__ __attribute__((aligned(16))) int s_seg[NBUF][BQ];
-  __shared__ __attribute__((aligned(16))) Frag s_p[2][4][NT][64];  // P handoff [buffer][key group][k step][lane]
+  __shared__ __attribute__((aligned(16))) Frag s_p[2][kKvGroups][NT][64];  // P handoff [buffer][group][k step][lane]
 
   const BlockSlot slot = xcd_slot(blockIdx.x, a.h_kv, 1);
   const int rank = slot.unit, kvh = slot.head;
@@ -103,8 +110,8 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
 
   const int tid = threadIdx.x, wave = uniform(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hh = lane >> 5;
-  const int grp = wave & 3;
-  const bool pwave = wave < 4;
+  const int grp = wave % kKvGroups;
+  const bool pwave = wave < kKvGroups;
   const int wk0 = td.row0 + 32 * grp;             // first key of this key group
   const bool wave_active = wk0 < td.row1;
   const int wk1 = min(wk0 + 32, td.row1) - 1;     // last valid key of the group
@@ -168,6 +175,10 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
   };
 
   TileLoader<T, BQ, D, kKvThreads> ldq, ldo;
+  ldq.init(a.h_q * D, tid);
+  ldo.init(a.h_q * D, tid);
+  FragOffsets<T, D> fo;
+  fo.init(lane);
   float pf_lse = 0.f, pf_dsum = 0.f;
   int pf_seg = 0;
   auto issue = [&](int it) {
@@ -175,8 +186,8 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
     const T* Qs = (const T*)(ti.qsuf ? a.q_suf : a.q_pre);
     const T* Gs = (const T*)(ti.qsuf ? a.do_suf : a.do_pre);
     const size_t off = ((size_t)ti.q0 * a.h_q + ti.hq) * D;
-    ldq.load(Qs + off, a.h_q * D, ti.qend - ti.q0, tid);
-    ldo.load(Gs + off, a.h_q * D, ti.qend - ti.q0, tid);
+    ldq.load(Qs + off, a.h_q * D, ti.qend - ti.q0);
+    ldo.load(Gs + off, a.h_q * D, ti.qend - ti.q0);
     if (tid < BQ) {
       const int q = ti.q0 + tid;
       const bool v = q < ti.qend;
@@ -188,8 +199,8 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
     }
   };
   auto commit = [&](int buf) {
-    ldq.store(smem[buf][0], tid);
-    ldo.store(smem[buf][1], tid);
+    ldq.store(smem[buf][0]);
+    ldo.store(smem[buf][1]);
     if (tid < BQ) { s_lse[buf][tid] = pf_lse; s_dsum[buf][tid] = pf_dsum; s_seg[buf][tid] = pf_seg; }
   };
 
@@ -209,10 +220,13 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
         const char* Gt = smem[buf][1];
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
+#ifdef PG_KV_SCHED_BARRIER
+          __builtin_amdgcn_sched_barrier(0);
+#endif
           f32x16 sc = f32x16{};
 #pragma unroll
           for (int kk = 0; kk < KK; ++kk)
-            sc = E::mma(E::template lds_row<D>(Qt, 32 * qb + n, 2 * kk + hh), kv[kk], sc);
+            sc = E::mma(fo.row(Qt, 32 * qb, kk), kv[kk], sc);
           // P = exp2(S*c - lse*log2e); rows are queries, the lane's column is its key
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
@@ -245,7 +259,7 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
             const Frag pf = E::acc_to_frag(sc, t2);
             s_p[it & 1][grp][t][lane] = pf;
 #pragma unroll
-            for (int db = 0; db < DB; ++db) acc[db] = E::mma(E::template lds_tr<D>(Gt, 16 * t, 32 * db, lane), pf, acc[db]);
+            for (int db = 0; db < DB; ++db) acc[db] = E::mma(fo.tr(Gt, t, db), pf, acc[db]);
           }
         }
       }
@@ -260,24 +274,27 @@ __global__ void __launch_bounds__(kKvThreads) dkdv_kernel(const BwdArgs a) {
         const char* Gt = smem[buf][1];
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
+#ifdef PG_KV_SCHED_BARRIER
+          __builtin_amdgcn_sched_barrier(0);
+#endif
           f32x16 dp = f32x16{};
 #pragma unroll
           for (int kk = 0; kk < KK; ++kk)
-            dp = E::mma(E::template lds_row<D>(Gt, 32 * qb + n, 2 * kk + hh), kv[kk], dp);
+            dp = E::mma(fo.row(Gt, 32 * qb, kk), kv[kk], dp);
 #pragma unroll
           for (int t2 = 0; t2 < 2; ++t2) {
             const int t = 2 * qb + t2;
             const Frag pf = s_p[(it - 1) & 1][grp][t][lane];
-            f32x16 ds;  // only registers [8 t2, 8 t2 + 8) are used
+            // registers 8 t2 + e, e = 0..7, hold query rows 32 qb + 8 (2 t2 + e/4) + 4 hh + e%4
+            const f32x4 d0 = *(const f32x4*)&s_dsum[buf][32 * qb + 16 * t2 + 4 * hh];
+            const f32x4 d1 = *(const f32x4*)&s_dsum[buf][32 * qb + 16 * t2 + 8 + 4 * hh];
+            float ds[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const int r = 8 * t2 + e;
-              const float d = s_dsum[buf][32 * qb + 8 * (r >> 2) + 4 * hh + (r & 3)];
-              ds[r] = E::frag_elem(pf, e) * (dp[r] - d);
-            }
-            const Frag dsf = E::acc_to_frag(ds, t2);
+            for (int e = 0; e < 8; ++e)
+              ds[e] = E::frag_elem(pf, e) * (dp[8 * t2 + e] - (e < 4 ? d0[e] : d1[e - 4]));
+            const Frag dsf = E::to_frag(ds);
 #pragma unroll
-            for (int db = 0; db < DB; ++db) acc[db] = E::mma(E::template lds_tr<D>(Qt, 16 * t, 32 * db, lane), dsf, acc[db]);
+            for (int db = 0; db < DB; ++db) acc[db] = E::mma(fo.tr(Qt, t, db), dsf, acc[db]);
           }
         }
       }
@@ -364,12 +381,16 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
   const int kvstride = a.h_kv * D;
 
   TileLoader<T, BN, D, kDqThreads> ldk, ldv;
+  ldk.init(kvstride, tid);
+  ldv.init(kvstride, tid);
+  FragOffsets<T, D> fo;
+  fo.init(lane);
   auto issue = [&](int j) {
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
-    ldk.load((segA ? Kp : Ks) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0, tid);
-    ldv.load((segA ? Vp : Vs) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0, tid);
+    ldk.load((segA ? Kp : Ks) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0);
+    ldv.load((segA ? Vp : Vs) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0);
   };
 
   f32x16 acc[DB];
@@ -379,8 +400,8 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
 
   if (ntiles > 0) {
     issue(0);
-    ldk.store(smem[0][0], tid);
-    ldv.store(smem[0][1], tid);
+    ldk.store(smem[0][0]);
+    ldv.store(smem[0][1]);
   }
   __syncthreads();
 
@@ -410,8 +431,8 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
         f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
-          s = E::mma(E::template lds_row<D>(Kt, 32 * kb + n, 2 * kk + hh), qf[kk], s);
-          dp = E::mma(E::template lds_row<D>(Vt, 32 * kb + n, 2 * kk + hh), gf[kk], dp);
+          s = E::mma(fo.row(Kt, 32 * kb, kk), qf[kk], s);
+          dp = E::mma(fo.row(Vt, 32 * kb, kk), gf[kk], dp);
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -437,13 +458,13 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
           const Frag dsf = E::acc_to_frag(dp, t2);
 #pragma unroll
           for (int db = 0; db < DB; ++db)
-            acc[db] = E::mma(E::template lds_tr<D>(Kt, 16 * (2 * kb + t2), 32 * db, lane), dsf, acc[db]);
+            acc[db] = E::mma(fo.tr(Kt, (2 * kb + t2), db), dsf, acc[db]);
         }
       }
     }
     if (j + 1 < ntiles) {
-      ldk.store(smem[buf ^ 1][0], tid);
-      ldv.store(smem[buf ^ 1][1], tid);
+      ldk.store(smem[buf ^ 1][0]);
+      ldv.store(smem[buf ^ 1][1]);
     }
     __syncthreads();
   }

@@ -103,26 +103,26 @@ __device__ __forceinline__ BlockSlot xcd_slot(int b, int heads, int per_kv) {
 }
 
 // ---------------------------------------------------------------- LDS tile addressing
-// A tile is `rows` rows of D elements, row-major. bf16 tiles use an unpadded pitch and
-// an XOR swizzle of their 16-byte chunks, chosen so that both access patterns of the
-// kernels are free of bank conflicts on the 64 x 4-byte LDS banks:
+// A tile is `rows` rows of D elements, row-major. bf16 rows are padded by 64 bytes
+// (four 16-byte chunks) and the low two bits of each chunk index are XORed with
+// (row >> 2) & 3. On the 64 x 4-byte LDS banks this keeps both access patterns of the
+// kernels free of conflicts:
 //  * row-fragment reads (ds_read_b128): 16 lanes read one chunk of 16 consecutive rows;
-//  * transposing reads (ds_read_b64_tr_b16): 32 lanes read 4 consecutive chunks of
-//    4 consecutive rows (row index a multiple of 4 at the start).
-// For 16-chunk rows (D = 128) the chunk of row r is XORed with 4(r&3) + ((r>>2)&3); for
-// 8-chunk rows (D = 64, two rows per bank line) with 4((r>>1)&1) + ((r>>2)&3). Both maps
-// send 16 consecutive rows to distinct bank groups for a fixed chunk, and 4 rows x 4
-// chunks to distinct bank groups. fp32 tiles keep a 16-byte row pad instead.
+//    the pad spreads rows 4 apart by four bank groups and the XOR separates the rows
+//    that wrap around;
+//  * transposing reads (ds_read_b64_tr_b16): 32 lanes read 4 consecutive chunks (one
+//    aligned group of 4) of 4 consecutive rows (starting at a multiple of 4).
+// Because the XOR only touches the low two chunk bits and repeats every 16 rows, the
+// offset of a fragment is a per-lane base plus compile-time multiples of 64 bytes and
+// of 16 rows, which the LDS instructions take as immediates. fp32 tiles keep a 16-byte
+// row pad instead.
 template <typename T, int D>
 struct LdsTile {
   static constexpr int kRowBytes = D * (int)sizeof(T);
   static constexpr int kChunks = kRowBytes / 16;
-  static constexpr bool kSwizzle = sizeof(T) == 2 && (kChunks == 16 || kChunks == 8);
-  static constexpr int kPitch = kSwizzle ? kRowBytes : kRowBytes + 16;
-  __device__ __forceinline__ static int swz(int row) {
-    if (!kSwizzle) return 0;
-    return kChunks == 16 ? (4 * (row & 3) + ((row >> 2) & 3)) : (4 * ((row >> 1) & 1) + ((row >> 2) & 3));
-  }
+  static constexpr bool kSwizzle = sizeof(T) == 2;
+  static constexpr int kPitch = kSwizzle ? kRowBytes + 64 : kRowBytes + 16;
+  __device__ __forceinline__ static int swz(int row) { return kSwizzle ? ((row >> 2) & 3) : 0; }
   // byte offset of 16-byte chunk `chunk` of row `row`
   __device__ __forceinline__ static int chunk_off(int row, int chunk) {
     return row * kPitch + 16 * (chunk ^ swz(row));
@@ -192,6 +192,12 @@ struct Elt<bf16> {
     return f;
   }
   __device__ __forceinline__ static float frag_elem(const Frag& f, int e) { return (float)f[e]; }
+  __device__ __forceinline__ static Frag to_frag(const float (&v)[8]) {
+    Frag f;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) f[s] = (bf16)v[s];
+    return f;
+  }
   __device__ __forceinline__ static void store4(bf16* p, float a, float b, float c, float d) {
     bf16x4 v = {(bf16)a, (bf16)b, (bf16)c, (bf16)d};
     *(bf16x4*)p = v;
@@ -251,41 +257,109 @@ struct Elt<float> {
     return f;
   }
   __device__ __forceinline__ static float frag_elem(const Frag& f, int e) { return f.v[e]; }
+  __device__ __forceinline__ static Frag to_frag(const float (&v)[8]) {
+    Frag f;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) f.v[s] = v[s];
+    return f;
+  }
   __device__ __forceinline__ static void store4(float* p, float a, float b, float c, float d) {
     *(f32x4*)p = f32x4{a, b, c, d};
   }
 };
 
-// Cooperative copy of `rows` rows of D elements (global row stride `gstride` elements)
-// into an LDS tile laid out by LdsTile<T, D>. Rows at or past `valid_rows` are
-// zero-filled. Done in two phases (load to registers, store to LDS) so the caller can
-// overlap the global latency with compute.
+// Cooperative copy of ROWS rows of D elements (global row stride `gstride` elements)
+// into an LDS tile laid out by LdsTile<T, D>, in two phases (load to registers, store
+// to LDS) so the caller can overlap the global latency with compute. Loads go through
+// a buffer resource whose range ends after the last valid row: rows past the end read
+// as zeros with no per-row test. Thread tid owns 16-byte chunk tid % C of rows
+// tid / C + i * (NT / C); its global and LDS offsets are affine in i (the swizzle
+// repeats every 16 rows), so they are computed once.
 template <typename T, int ROWS, int D, int NT>
 struct TileLoader {
   static constexpr int kChunks = D * (int)sizeof(T) / 16;  // 16-byte chunks per row
   static constexpr int kTotal = ROWS * kChunks;
-  static constexpr int kPer = (kTotal + NT - 1) / NT;
-  static_assert(kTotal % NT == 0, "tile must split evenly over the threads");
+  static constexpr bool kPartial = kTotal < NT;              // fewer chunks than threads
+  static constexpr int kPer = kPartial ? 1 : kTotal / NT;
+  static constexpr int kRowStep = kPartial ? ROWS : NT / kChunks;  // rows between a thread's chunks
+  static_assert((kPartial || (kTotal % NT == 0 && NT % kChunks == 0)) &&
+                    (!LdsTile<T, D>::kSwizzle || kPer == 1 || kRowStep % 16 == 0),
+                "tile/threads mismatch");
   uint4 reg[kPer];
-  __device__ __forceinline__ void load(const T* base, int gstride, int valid_rows, int tid) {
-    // rows past the end are read from the last valid row and replaced by zeros (no branches)
+  int goff, loff, gstep;
+  bool active;
+  __device__ __forceinline__ void init(int gstride, int tid) {
+    const int r = tid / kChunks, k = tid % kChunks;
+    active = !kPartial || tid < kTotal;
+    gstep = kRowStep * gstride * (int)sizeof(T);
+    goff = r * gstride * (int)sizeof(T) + 16 * k;
+    loff = LdsTile<T, D>::chunk_off(r, k);
+  }
+  __device__ __forceinline__ void load(const T* base, int gstride, int valid_rows) {
+    const int bytes = valid_rows * gstride * (int)sizeof(T);
+    __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, bytes, 0x00020000);
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
-      const int c = tid + i * NT;
-      const int r = c / kChunks, k = c % kChunks;
-      const int rc = r < valid_rows ? r : valid_rows - 1;
-      const uint4 v = *(const uint4*)((const char*)(base + (size_t)rc * gstride) + 16 * k);
-      const bool ok = r < valid_rows;
-      reg[i] = uint4{ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u};
+      if (active) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, goff + i * gstep, 0, 0);
+        reg[i] = __builtin_bit_cast(uint4, v);
+      }
     }
   }
-  __device__ __forceinline__ void store(char* lds, int tid) const {
+  __device__ __forceinline__ void store(char* lds) const {
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int c = tid + i * NT;
-      const int r = c / kChunks, k = c % kChunks;
-      *(uint4*)(lds + LdsTile<T, D>::chunk_off(r, k)) = reg[i];
-    }
+    for (int i = 0; i < kPer; ++i)
+      if (active) *(uint4*)(lds + loff + i * kRowStep * LdsTile<T, D>::kPitch) = reg[i];
+  }
+};
+
+// Per-lane LDS offsets of the MFMA operand fragments, computed once per kernel.
+//   row(tile, row_base, kk)  : row fragment of row row_base + lane%32 (row_base a multiple
+//                              of 16), elements 16 kk + 8 (lane/32) .. +8;
+//   tr(tile, t, db)          : transposed fragment (see Elt::lds_tr) for rows 16 t .., and
+//                              columns 32 db + lane%32.
+// bf16 tiles keep the offsets in registers (the swizzle repeats every 16 rows, so row
+// and k-step offsets become immediates); fp32 tiles compute them on the fly.
+template <typename T, int D>
+struct FragOffsets;
+
+template <int D>
+struct FragOffsets<bf16, D> {
+  using E = Elt<bf16>;
+  using L = LdsTile<bf16, D>;
+  int row_[2];  // row fragment, k steps with kk even / odd (kk >> 1 adds 64 bytes)
+  int tr_[2];   // transposed fragment, first / second 4-row read (d block adds 64 bytes)
+  __device__ __forceinline__ void init(int lane) {
+    const int n = lane & 31, hh = lane >> 5;
+    const int g16 = (lane & 31) >> 4, j = lane & 15;
+    row_[0] = L::chunk_off(n, hh);
+    row_[1] = L::chunk_off(n, 2 + hh);
+    tr_[0] = L::elem_off(4 * hh + (j >> 2), 16 * g16 + 4 * (j & 3));
+    tr_[1] = L::elem_off(4 * hh + (j >> 2) + 8, 16 * g16 + 4 * (j & 3));
+  }
+  __device__ __forceinline__ E::Frag row(const char* tile, int row_base, int kk) const {
+    return *(const E::Frag*)(tile + row_[kk & 1] + 64 * (kk >> 1) + row_base * L::kPitch);
+  }
+  __device__ __forceinline__ E::Frag tr(const char* tile, int t, int db) const {
+    const char* p0 = tile + tr_[0] + 64 * db + 16 * t * L::kPitch;
+    const char* p1 = tile + tr_[1] + 64 * db + 16 * t * L::kPitch;
+    i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p0));
+    i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p1));
+    i16x8 ab = __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(E::Frag, ab);
+  }
+};
+
+template <int D>
+struct FragOffsets<float, D> {
+  using E = Elt<float>;
+  int lane_;
+  __device__ __forceinline__ void init(int lane) { lane_ = lane; }
+  __device__ __forceinline__ E::Frag row(const char* tile, int row_base, int kk) const {
+    return E::template lds_row<D>(tile, row_base + (lane_ & 31), 2 * kk + (lane_ >> 5));
+  }
+  __device__ __forceinline__ E::Frag tr(const char* tile, int t, int db) const {
+    return E::template lds_tr<D>(tile, 16 * t, 32 * db, lane_);
   }
 };
 

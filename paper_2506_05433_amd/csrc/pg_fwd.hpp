@@ -89,14 +89,18 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
   const int kvstride = a.h_kv * D;
 
   TileLoader<T, BN, D, kFwdThreads> ldk, ldv;
+  ldk.init(kvstride, tid);
+  ldv.init(kvstride, tid);
+  FragOffsets<T, D> fo;
+  fo.init(lane);
   auto issue = [&](int j) {
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
     const T* kb = (segA ? Kp : Ks) + (size_t)k0 * kvstride + kvh * D;
     const T* vb = (segA ? Vp : Vs) + (size_t)k0 * kvstride + kvh * D;
-    ldk.load(kb, kvstride, kend - k0, tid);
-    ldv.load(vb, kvstride, kend - k0, tid);
+    ldk.load(kb, kvstride, kend - k0);
+    ldv.load(vb, kvstride, kend - k0);
   };
 
   f32x16 acc_o[DB];
@@ -107,8 +111,8 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
 
   if (ntiles > 0) {
     issue(0);
-    ldk.store(smem[0][0], tid);
-    ldv.store(smem[0][1], tid);
+    ldk.store(smem[0][0]);
+    ldv.store(smem[0][1]);
   }
   __syncthreads();
 
@@ -140,7 +144,7 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
         s[kb] = f32x16{};
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk)
-          s[kb] = E::mma(E::template lds_row<D>(Kt, 32 * kb + n, 2 * kk + hh), qf[kk], s[kb]);
+          s[kb] = E::mma(fo.row(Kt, 32 * kb, kk), qf[kk], s[kb]);
       }
       // Mask, only on tiles that straddle a boundary (a real branch: the empty asm keeps
       // the compiler from turning it into selects executed on every tile). Key offset
@@ -195,14 +199,14 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
         const Frag pf = E::acc_to_frag(s[t >> 1], t & 1);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const Frag vf = E::template lds_tr<D>(Vt, 16 * t, 32 * db, lane);
+          const Frag vf = fo.tr(Vt, t, db);
           acc_o[db] = E::mma(vf, pf, acc_o[db]);
         }
       }
     }
     if (j + 1 < ntiles) {
-      ldk.store(smem[buf ^ 1][0], tid);
-      ldv.store(smem[buf ^ 1][1], tid);
+      ldk.store(smem[buf ^ 1][0]);
+      ldv.store(smem[buf ^ 1][1]);
     }
     __syncthreads();
   }
