@@ -11,6 +11,8 @@ counted. The same kernels are also timed on the repeated-prefix layout
 (every member with its own copy of the prefix) for the speedup.
 """
 import argparse
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -119,6 +121,45 @@ def cpu_baseline(prob, useful_per_pair_head, budget_s):
             "seconds": dt, "host_cpus": len(os.sched_getaffinity(0))}
 
 
+def kernel_source_sha():
+    """Digest of the HIP sources: counter readings are only reported for the build they were taken on."""
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2506_05433_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(kernel, workload):
+    """HBM bytes per launch from profiles/traffic_<kernel>_<workload>.json if taken on this source, else None.
+
+    The file holds rocprofv3 FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the kernel and of a plain
+    device copy of known size; each counter is scaled by copy_bytes / counter(copy).
+    """
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        t = json.load(fh)
+    if t.get("source_sha") != kernel_source_sha():
+        return None
+    f = t["fetch_kib"] * t["copy_read_bytes"] / t["copy_fetch_kib"]
+    w = t["write_kib"] * t["copy_write_bytes"] / t["copy_write_kib"]
+    return f + w
+
+
+def calibrate_copy(n_bytes):
+    """A plain device-to-device copy of n_bytes (reference reading for the HBM byte counters)."""
+    import torch
+    src = torch.empty(n_bytes // 4, device="cuda", dtype=torch.float32).fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n_bytes, "launches": 3}))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -128,11 +169,17 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-repeated", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
 
     import torch
 
@@ -170,7 +217,8 @@ def main():
         "bwd_tflops": round(bwd_flops / (bwd_ms * 1e-3) / 1e12, 2) if bwd_ms else None,
         "kernels_ms": {k: (round(v["avg_ms"], 4) if v["avg_ms"] else None) for k, v in kern.items()},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
-                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None},
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                     "traffic": recorded_traffic(dom, wl.name), "source_sha": kernel_source_sha()},
     }
     if not args.no_repeated:
         rep = repeated_layout(prob)

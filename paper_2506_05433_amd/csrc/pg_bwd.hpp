@@ -132,15 +132,18 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
   for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
 
   // Query ranges that see these keys, in fixed order:
-  //   prefix keys  : prefix rows [row0, p1) (causal), then response rows [s0, s1) (dense)
-  //   response keys: response rows [row0, aux) (causal within each member)
-  const int r1_lo = td.row0;
-  const int r1_hi = kv_suffix ? td.aux : gi.p1;
-  const int r2_lo = kv_suffix ? 0 : gi.s0;
-  const int r2_hi = kv_suffix ? 0 : gi.s1;
-  const int n1 = (r1_hi - r1_lo + BQ - 1) / BQ;
-  const int n2 = (r2_hi - r2_lo + BQ - 1) / BQ;
-  const int per_head = n1 + n2;
+  //   prefix keys  : response rows [s0, s1) (dense), then prefix rows [row0, p1) (causal);
+  //   response keys: response rows [row0, aux) (causal within each member).
+  // The dense response range comes first so that the workgroups of all prefix key
+  // tiles of a kv head, which start together, stream the same query tiles in step
+  // and share them in L2.
+  const int rc_lo = td.row0;                       // causal range
+  const int rc_hi = kv_suffix ? td.aux : gi.p1;
+  const int rd_lo = kv_suffix ? 0 : gi.s0;         // dense range
+  const int rd_hi = kv_suffix ? 0 : gi.s1;
+  const int nd = (rd_hi - rd_lo + BQ - 1) / BQ;
+  const int nc = (rc_hi - rc_lo + BQ - 1) / BQ;
+  const int per_head = nd + nc;
   const int total = per_head * ratio;
   const float c = a.scale_log2;
 
@@ -152,11 +155,10 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     TileInfo ti;
     ti.hq = kvh * ratio + it / per_head;
     const int j = it % per_head;
-    const bool first = j < n1;
-    ti.qsuf = first ? kv_suffix : true;
-    ti.q0 = first ? r1_lo + j * BQ : r2_lo + (j - n1) * BQ;
-    ti.qend = first ? r1_hi : r2_hi;
-    ti.causal = first;  // prefix keys x prefix rows, or response keys x response rows
+    ti.causal = j >= nd;  // prefix keys x prefix rows, or response keys x response rows
+    ti.qsuf = ti.causal ? kv_suffix : true;
+    ti.q0 = ti.causal ? rc_lo + (j - nd) * BQ : rd_lo + j * BQ;
+    ti.qend = ti.causal ? rc_hi : rd_hi;
     return ti;
   };
   // visibility of a tile to this key group: skip (no pair visible) / full (all visible)
