@@ -176,9 +176,9 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     }
   };
 
-  TileLoader<T, BQ, D, kKvThreads> ldq, ldo;
-  ldq.init(a.h_q * D, tid);
-  ldo.init(a.h_q * D, tid);
+  Stager<T, BQ, D, kKvThreads> ldq, ldo;
+  ldq.init(a.h_q * D, wave, lane);
+  ldo.init(a.h_q * D, wave, lane);
   FragOffsets<T, D> fo;
   fo.init(lane);
   float pf_lse = 0.f, pf_dsum = 0.f;
@@ -188,8 +188,8 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     const T* Qs = (const T*)(ti.qsuf ? a.q_suf : a.q_pre);
     const T* Gs = (const T*)(ti.qsuf ? a.do_suf : a.do_pre);
     const size_t off = ((size_t)ti.q0 * a.h_q + ti.hq) * D;
-    ldq.load(Qs + off, a.h_q * D, ti.qend - ti.q0);
-    ldo.load(Gs + off, a.h_q * D, ti.qend - ti.q0);
+    ldq.load(smem[it % NBUF][0], Qs + off, a.h_q * D, ti.qend - ti.q0);
+    ldo.load(smem[it % NBUF][1], Gs + off, a.h_q * D, ti.qend - ti.q0);
     if (tid < BQ) {
       const int q = ti.q0 + tid;
       const bool v = q < ti.qend;
@@ -207,6 +207,7 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
   };
 
   if (total > 0) { issue(0); commit(0); }
+  ldq.wait();
   __syncthreads();
 
   for (int it = 0; it <= total; ++it) {
@@ -302,6 +303,7 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
       }
     }
     if (it + 1 < total) commit((it + 1) % NBUF);
+    ldq.wait();
     __syncthreads();
   }
 
@@ -382,17 +384,17 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
   const T* Ks = (const T*)a.k_suf; const T* Vs = (const T*)a.v_suf;
   const int kvstride = a.h_kv * D;
 
-  TileLoader<T, BN, D, kDqThreads> ldk, ldv;
-  ldk.init(kvstride, tid);
-  ldv.init(kvstride, tid);
+  Stager<T, BN, D, kDqThreads> ldk, ldv;
+  ldk.init(kvstride, wave, lane);
+  ldv.init(kvstride, wave, lane);
   FragOffsets<T, D> fo;
   fo.init(lane);
   auto issue = [&](int j) {
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
-    ldk.load((segA ? Kp : Ks) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0);
-    ldv.load((segA ? Vp : Vs) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0);
+    ldk.load(smem[j & 1][0], (segA ? Kp : Ks) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0);
+    ldv.load(smem[j & 1][1], (segA ? Vp : Vs) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0);
   };
 
   f32x16 acc[DB];
@@ -405,6 +407,7 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
     ldk.store(smem[0][0]);
     ldv.store(smem[0][1]);
   }
+  ldk.wait();
   __syncthreads();
 
   for (int j = 0; j < ntiles; ++j) {
@@ -468,6 +471,7 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
       ldk.store(smem[buf ^ 1][0]);
       ldv.store(smem[buf ^ 1][1]);
     }
+    ldk.wait();
     __syncthreads();
   }
 

@@ -288,14 +288,15 @@ struct TileLoader {
   uint4 reg[kPer];
   int goff, loff, gstep;
   bool active;
-  __device__ __forceinline__ void init(int gstride, int tid) {
+  __device__ __forceinline__ void init(int gstride, int wave, int lane) {
+    const int tid = 64 * wave + lane;
     const int r = tid / kChunks, k = tid % kChunks;
     active = !kPartial || tid < kTotal;
     gstep = kRowStep * gstride * (int)sizeof(T);
     goff = r * gstride * (int)sizeof(T) + 16 * k;
     loff = LdsTile<T, D>::chunk_off(r, k);
   }
-  __device__ __forceinline__ void load(const T* base, int gstride, int valid_rows) {
+  __device__ __forceinline__ void load(char* /*lds*/, const T* base, int gstride, int valid_rows) {
     const int bytes = valid_rows * gstride * (int)sizeof(T);
     __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, bytes, 0x00020000);
 #pragma unroll
@@ -311,7 +312,67 @@ struct TileLoader {
     for (int i = 0; i < kPer; ++i)
       if (active) *(uint4*)(lds + loff + i * kRowStep * LdsTile<T, D>::kPitch) = reg[i];
   }
+  __device__ __forceinline__ void wait() const {}
 };
+
+// bf16 tiles are copied global -> LDS directly (buffer_load ... lds, 16 bytes per lane): no
+// registers are held and no LDS store is issued. One wave instruction fills 1 KiB of LDS
+// starting at the address given for the whole wave, lane i writing bytes [16i, 16i+16), so
+// each lane fetches the global chunk that belongs at its LDS position in the padded,
+// swizzled layout; lanes that land on row padding (and rows past the end) fetch from beyond
+// the buffer's range and store zeros. wait() must precede the barrier that publishes the tile.
+// 16 bytes per lane from a buffer into LDS at `lds` + 16 * lane (lds is wave-uniform).
+// The builtin only exists for the device; the host pass of this file sees an empty body
+// (it would otherwise drop the host launch stubs of some kernels that use it).
+__device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t rs, char* lds, int voff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds, 16, voff, 0, 0, 0);
+#endif
+}
+
+template <int ROWS, int D, int NWAVES>
+struct DirectLoader {
+  using L = LdsTile<bf16, D>;
+  static constexpr int kBytes = ROWS * L::kPitch;
+  static constexpr int kInstr = kBytes / 1024;                       // wave instructions per tile
+  static constexpr int kPerWave = (kInstr + NWAVES - 1) / NWAVES;
+  static_assert(kBytes % 1024 == 0, "tile must be a whole number of KiB");
+  static constexpr int kOutOfRange = 0x7ffffff0;
+  int voff[kPerWave];
+  int wave_;
+  __device__ __forceinline__ void init(int gstride, int wave, int lane) {
+    wave_ = wave;
+#pragma unroll
+    for (int k = 0; k < kPerWave; ++k) {
+      const int p = 1024 * (wave + k * NWAVES) + 16 * lane;  // LDS byte this lane fills
+      const int row = p / L::kPitch, pc = (p % L::kPitch) / 16;
+      voff[k] = (pc < L::kChunks && p < kBytes) ? row * gstride * 2 + 16 * (pc ^ L::swz(row)) : kOutOfRange;
+    }
+  }
+  __device__ __forceinline__ void load(char* lds, const bf16* base, int gstride, int valid_rows) {
+    const int bytes = valid_rows * gstride * 2;
+    __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, bytes, 0x00020000);
+#pragma unroll
+    for (int k = 0; k < kPerWave; ++k) {
+      const int w = wave_ + k * NWAVES;
+      if (w < kInstr) lds_dma16(rs, lds + 1024 * w, voff[k]);
+    }
+  }
+  __device__ __forceinline__ void store(char* /*lds*/) const {}
+  __device__ __forceinline__ void wait() const { __builtin_amdgcn_s_waitcnt(0); }
+};
+
+// Stager<T, ROWS, D, NT>: the tile copier a kernel with NT threads uses for element type T.
+template <typename T, int ROWS, int D, int NT>
+struct StagerSel {
+  using type = TileLoader<T, ROWS, D, NT>;
+};
+template <int ROWS, int D, int NT>
+struct StagerSel<bf16, ROWS, D, NT> {
+  using type = DirectLoader<ROWS, D, NT / 64>;
+};
+template <typename T, int ROWS, int D, int NT>
+using Stager = typename StagerSel<T, ROWS, D, NT>::type;
 
 // Per-lane LDS offsets of the MFMA operand fragments, computed once per kernel.
 //   row(tile, row_base, kk)  : row fragment of row row_base + lane%32 (row_base a multiple

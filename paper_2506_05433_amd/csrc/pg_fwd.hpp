@@ -88,9 +88,9 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
   const T* Ks = (const T*)a.k_suf; const T* Vs = (const T*)a.v_suf;
   const int kvstride = a.h_kv * D;
 
-  TileLoader<T, BN, D, kFwdThreads> ldk, ldv;
-  ldk.init(kvstride, tid);
-  ldv.init(kvstride, tid);
+  Stager<T, BN, D, kFwdThreads> ldk, ldv;
+  ldk.init(kvstride, wave, lane);
+  ldv.init(kvstride, wave, lane);
   FragOffsets<T, D> fo;
   fo.init(lane);
   auto issue = [&](int j) {
@@ -99,8 +99,8 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
     const int kend = segA ? kA1 : kB1;
     const T* kb = (segA ? Kp : Ks) + (size_t)k0 * kvstride + kvh * D;
     const T* vb = (segA ? Vp : Vs) + (size_t)k0 * kvstride + kvh * D;
-    ldk.load(kb, kvstride, kend - k0);
-    ldv.load(vb, kvstride, kend - k0);
+    ldk.load(smem[j & 1][0], kb, kvstride, kend - k0);
+    ldv.load(smem[j & 1][1], vb, kvstride, kend - k0);
   };
 
   f32x16 acc_o[DB];
@@ -114,6 +114,7 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
     ldk.store(smem[0][0]);
     ldv.store(smem[0][1]);
   }
+  ldk.wait();
   __syncthreads();
 
   for (int j = 0; j < ntiles; ++j) {
@@ -208,6 +209,7 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
       ldk.store(smem[buf ^ 1][0]);
       ldv.store(smem[buf ^ 1][1]);
     }
+    ldk.wait();
     __syncthreads();
   }
 
