@@ -151,10 +151,11 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     int hq, q0, qend;
     bool qsuf, causal;
   };
-  auto info = [&](int it) {
+  // tile `it` is position j of query head hd's walk; the loop advances (hd, j) by one
+  // tile per iteration instead of dividing
+  auto info = [&](int hd, int j) {
     TileInfo ti;
-    ti.hq = kvh * ratio + it / per_head;
-    const int j = it % per_head;
+    ti.hq = kvh * ratio + hd;
     ti.causal = j >= nd;  // prefix keys x prefix rows, or response keys x response rows
     ti.qsuf = ti.causal ? kv_suffix : true;
     ti.q0 = ti.causal ? rc_lo + (j - nd) * BQ : rd_lo + j * BQ;
@@ -183,8 +184,7 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
   fo.init(lane);
   float pf_lse = 0.f, pf_dsum = 0.f;
   int pf_seg = 0;
-  auto issue = [&](int it) {
-    const TileInfo ti = info(it);
+  auto issue = [&](const TileInfo& ti, int it) {
     const T* Qs = (const T*)(ti.qsuf ? a.q_suf : a.q_pre);
     const T* Gs = (const T*)(ti.qsuf ? a.do_suf : a.do_pre);
     const size_t off = ((size_t)ti.q0 * a.h_q + ti.hq) * D;
@@ -206,16 +206,21 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     if (tid < BQ) { s_lse[buf][tid] = pf_lse; s_dsum[buf][tid] = pf_dsum; s_seg[buf][tid] = pf_seg; }
   };
 
-  if (total > 0) { issue(0); commit(0); }
+  TileInfo ti_cur = info(0, 0), ti_prev = ti_cur;  // tiles it and it - 1
+  int cur_hd = 0, cur_j = 0;
+  if (total > 0) { issue(ti_cur, 0); commit(0); }
   ldq.wait();
   __syncthreads();
 
   for (int it = 0; it <= total; ++it) {
-    if (it + 1 < total) issue(it + 1);
+    int nxt_hd = cur_hd, nxt_j = cur_j + 1;
+    if (nxt_j == per_head) { nxt_j = 0; ++nxt_hd; }
+    const TileInfo ti_next = info(nxt_hd, nxt_j);
+    if (it + 1 < total) issue(ti_next, it + 1);
     if (pwave && it < total && wave_active) {
       // ---------------- P-wave on tile it
       const int buf = it % NBUF;
-      const TileInfo ti = info(it);
+      const TileInfo& ti = ti_cur;
       bool skip, full;
       visibility(ti, buf, skip, full);
       if (!skip) {
@@ -269,7 +274,7 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     } else if (!pwave && it > 0 && wave_active) {
       // ---------------- G-wave on tile it-1
       const int buf = (it - 1) % NBUF;
-      const TileInfo ti = info(it - 1);
+      const TileInfo& ti = ti_prev;
       bool skip, full;
       visibility(ti, buf, skip, full);
       if (!skip) {
@@ -303,6 +308,10 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
       }
     }
     if (it + 1 < total) commit((it + 1) % NBUF);
+    ti_prev = ti_cur;
+    ti_cur = ti_next;
+    cur_hd = nxt_hd;
+    cur_j = nxt_j;
     ldq.wait();
     __syncthreads();
   }

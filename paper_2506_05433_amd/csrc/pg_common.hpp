@@ -402,8 +402,12 @@ struct FragOffsets<bf16, D> {
     return *(const E::Frag*)(tile + row_[kk & 1] + 64 * (kk >> 1) + row_base * L::kPitch);
   }
   __device__ __forceinline__ E::Frag tr(const char* tile, int t, int db) const {
-    const char* p0 = tile + tr_[0] + 64 * db + 16 * t * L::kPitch;
-    const char* p1 = tile + tr_[1] + 64 * db + 16 * t * L::kPitch;
+    // address arithmetic in the LDS address space, so the constant part becomes the
+    // instruction's offset field
+    typedef __attribute__((address_space(3))) const char lds_char;
+    lds_char* base = (lds_char*)tile;
+    lds_char* p0 = base + tr_[0] + (64 * db + 16 * t * L::kPitch);
+    lds_char* p1 = base + tr_[1] + (64 * db + 16 * t * L::kPitch);
     i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p0));
     i16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p1));
     i16x8 ab = __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
