@@ -93,32 +93,34 @@ def alloc(binding, torch, dev, prob):
 
 
 def cpu_baseline(prob, useful_per_pair_head, budget_s):
-    """The oracle (fp64 numpy, as it stands) on a bounded sample: all rows, a few query heads."""
+    """The oracle (fp64 numpy, as it stands) on a bounded sample of the workload.
+
+    The sample is all rows and members of the first k query heads, fwd+bwd; one head is
+    timed first and k is chosen so the measured run takes about ``budget_s`` seconds.
+    """
     import numpy as np
     from threadpoolctl import threadpool_info
 
     from oracle import grouped_oracle
-    n_heads = 1
     t = {k: prob.as_float(k, np.float64) for k in prob.tensors}
     pairs_rep = repeated_pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
     pairs = pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
-    t0 = time.perf_counter()
-    grouped_oracle(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, grads=True,
-                   heads=list(range(n_heads)), check_members=False)
-    dt = time.perf_counter() - t0
-    # grow the sample toward the budget if the first head was quick
-    if dt < budget_s / 3 and prob.h_q > 1:
-        n_heads = max(1, min(prob.h_q, int(budget_s / max(dt, 1e-3) * 0.5)))
+
+    def run(n):
         t0 = time.perf_counter()
         grouped_oracle(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, grads=True,
-                       heads=list(range(n_heads)), check_members=False)
-        dt = time.perf_counter() - t0
+                       heads=list(range(n)), check_members=False)
+        return time.perf_counter() - t0
+
+    dt1 = run(1)
+    n_heads = max(1, min(prob.h_q, int(budget_s / max(dt1, 1e-3))))
+    dt = run(n_heads) if n_heads > 1 else dt1
     useful = useful_per_pair_head * pairs * n_heads
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {"value": useful / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{n_heads} of {prob.h_q} query heads, all rows and members, fp64 numpy, repeated-prefix "
                       f"({pairs_rep} repeated pairs per head), fwd+bwd; {dt:.1f} s",
-            "seconds": dt, "host_cpus": len(os.sched_getaffinity(0))}
+            "seconds": round(dt, 2), "host_cpus": len(os.sched_getaffinity(0))}
 
 
 def kernel_source_sha():
@@ -168,7 +170,7 @@ def main():
     ap.add_argument("--workload", default="single_group")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-repeated", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES (counter calibration)")
     args = ap.parse_args()

@@ -97,6 +97,10 @@ SMALL = [
     (((129, 0), (2, 2), (40, 63, 1, 128)), 2, 1, 64, "fp32"),
     (((0,), (1,), (5,)), 2, 2, 64, "bf16"),
     (((7,), (0,), ()), 2, 1, 128, "bf16"),
+    # many groups: empty groups, a group without prefix, prefixes shorter than a tile, GQA ratio 8
+    (((3, 0, 200, 1), (2, 1, 0, 3), (5, 0, 7, 1, 1, 130)), 8, 1, 128, "bf16"),
+    # GQA ratio 5 with head_dim 64
+    (((150,), (2,), (77, 200)), 5, 1, 64, "bf16"),
 ]
 
 
