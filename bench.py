@@ -86,7 +86,8 @@ def alloc(binding, torch, dev, prob):
                 torch.empty((prob.h_q, prob.total_suffix), device="cuda", dtype=torch.float32)),
         "bwd": tuple(torch.empty_like(dev[k]) for k in ("q_pre", "k_pre", "v_pre", "q_suf", "k_suf", "v_suf")),
     }
-    args = (len(prob.prefix_lens), len(prob.suffix_lens), prob.total_prefix, prob.total_suffix, prob.h_q)
+    args = (len(prob.prefix_lens), len(prob.suffix_lens), prob.total_prefix, prob.total_suffix, prob.h_q, prob.h_kv,
+            prob.head_dim)
     bufs["ws_f"] = torch.empty(binding.workspace_bytes("fwd", *args), device="cuda", dtype=torch.uint8)
     bufs["ws_b"] = torch.empty(binding.workspace_bytes("bwd", *args), device="cuda", dtype=torch.uint8)
     return bufs

@@ -68,11 +68,15 @@ typedef enum {
   PG_EHIP = 4          /* HIP runtime failure (no device, launch error, ...)           */
 } pg_status;
 
-/* Workspace bytes pg_attn_fwd needs for these sizes (host call, no GPU use). */
-size_t pg_attn_fwd_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q);
+/* Workspace bytes pg_attn_fwd needs for these sizes (host call, no GPU use; 0 for negative sizes). */
+size_t pg_attn_fwd_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q,
+                                  int h_kv, int head_dim);
 
-/* Workspace bytes pg_attn_bwd needs for these sizes (host call, no GPU use). */
-size_t pg_attn_bwd_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q);
+/* Workspace bytes pg_attn_bwd needs for these sizes (host call, no GPU use; 0 for negative sizes). It holds
+ * the tile plan, rowsum(dO*O) and, when the walks of long prefix key tiles are split over several workgroups,
+ * their fp32 dK/dV partial sums. */
+size_t pg_attn_bwd_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q,
+                                  int h_kv, int head_dim);
 
 /*
  * Forward pass: Eq. (4). Writes o_pre, o_suf and the natural-log

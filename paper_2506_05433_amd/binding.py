@@ -22,8 +22,8 @@ _lib = None
 # names and argument types of every function include/pg_attn.h declares
 _I, _Z, _F, _P = ctypes.c_int, ctypes.c_size_t, ctypes.c_float, ctypes.c_void_p
 SIGNATURES = {
-    "pg_attn_fwd_workspace_size": (_Z, [_I, _I, _I, _I, _I]),
-    "pg_attn_bwd_workspace_size": (_Z, [_I, _I, _I, _I, _I]),
+    "pg_attn_fwd_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
+    "pg_attn_bwd_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
     "pg_attn_fwd": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 10 + [_P, _Z, _P]),
     "pg_attn_bwd": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 18 + [_P, _Z, _P]),
     "pg_timing_start": (_I, []),
@@ -94,9 +94,9 @@ def _stream(torch, device):
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
-def workspace_bytes(kind: str, n_groups, n_suffixes, total_prefix, total_suffix, h_q) -> int:
+def workspace_bytes(kind: str, n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim) -> int:
     fn = lib().pg_attn_fwd_workspace_size if kind == "fwd" else lib().pg_attn_bwd_workspace_size
-    return int(fn(n_groups, n_suffixes, total_prefix, total_suffix, h_q))
+    return int(fn(n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim))
 
 
 def _shapes(q_pre, k_pre, q_suf, cu_prefix, cu_suffix, group_sizes):
@@ -120,7 +120,7 @@ def fwd(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, cu_prefix, cu_suffix, group_si
         out = (torch.empty_like(q_pre), torch.empty_like(q_suf),
                torch.empty((hq, tp), device=dev, dtype=torch.float32),
                torch.empty((hq, ts), device=dev, dtype=torch.float32))
-    need = workspace_bytes("fwd", ng, ns, tp, ts, hq)
+    need = workspace_bytes("fwd", ng, ns, tp, ts, hq, hkv, d)
     if workspace is None:
         workspace = torch.empty(need, device=dev, dtype=torch.uint8)
     o_pre, o_suf, lse_pre, lse_suf = out
@@ -143,7 +143,7 @@ def bwd(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, o_pre, o_suf, lse_pre, lse_suf
     if out is None:
         out = (torch.empty_like(q_pre), torch.empty_like(k_pre), torch.empty_like(v_pre),
                torch.empty_like(q_suf), torch.empty_like(k_suf), torch.empty_like(v_suf))
-    need = workspace_bytes("bwd", ng, ns, tp, ts, hq)
+    need = workspace_bytes("bwd", ng, ns, tp, ts, hq, hkv, d)
     if workspace is None:
         workspace = torch.empty(need, device=dev, dtype=torch.uint8)
     st = lib().pg_attn_bwd(

@@ -38,15 +38,27 @@ long ceil_div_l(long a, long b) { return (a + b - 1) / b; }
 
 // Workspace layout shared by the forward and backward calls.
 struct Layout {
-  size_t hdr, ginfo, qoff, kvoff, qtiles, qorder, kvtiles, kvorder, seg, dsum, total;
+  size_t hdr, ginfo, qoff, kvoff, qtiles, qorder, kvtiles, kvorder, seg, dsum, part, total;
   long max_q, max_kv;
+  int kv_chunks;
 };
 
-Layout make_layout(int ng, int ns, int tp, int ts, int h_q, bool bwd) {
+// Pieces each prefix key tile's query walk is split into for the dK/dV kernel: enough
+// workgroups to balance the long prefix walks over the CUs (about 1024 prefix pieces),
+// at most 8, and 1 when there are already that many prefix key tiles.
+int kv_chunks_for(int ng, int tp, int h_kv) {
+  if (tp <= 0 || h_kv <= 0) return 1;
+  const long tiles = (ceil_div_l(tp, pg::kKvBN) + ng) * (long)h_kv;
+  const long c = ceil_div_l(1024, tiles);
+  return (int)(c < 1 ? 1 : (c > 8 ? 8 : c));
+}
+
+Layout make_layout(int ng, int ns, int tp, int ts, int h_q, int h_kv, int d, bool bwd) {
   (void)ns;
   Layout L{};
+  L.kv_chunks = bwd ? kv_chunks_for(ng, tp, h_kv) : 1;
   L.max_q = ceil_div_l(tp, pg::kFwdBM) + ceil_div_l(ts, pg::kFwdBM) + 2L * ng;
-  L.max_kv = bwd ? ceil_div_l(tp, pg::kKvBN) + ceil_div_l(ts, pg::kKvBN) + 2L * ng : 0;
+  L.max_kv = bwd ? (ceil_div_l(tp, pg::kKvBN) + ng) * L.kv_chunks + ceil_div_l(ts, pg::kKvBN) + ng : 0;
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
   L.hdr = take(sizeof(pg::PlanHeader));
@@ -59,6 +71,7 @@ Layout make_layout(int ng, int ns, int tp, int ts, int h_q, bool bwd) {
   L.kvorder = take(sizeof(int) * (size_t)(L.max_kv > 0 ? L.max_kv : 1));
   L.seg = take(sizeof(int) * (size_t)(ts > 0 ? ts : 1));
   L.dsum = bwd ? take(sizeof(float) * (size_t)h_q * (size_t)(tp + ts > 0 ? tp + ts : 1)) : off;
+  L.part = (bwd && L.kv_chunks > 1) ? take(sizeof(float) * (size_t)L.kv_chunks * 2 * tp * h_kv * d) : off;
   L.total = off;
   return L;
 }
@@ -155,14 +168,14 @@ int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p,
   int* qoff = (int*)(ws + L.qoff);
   int* kvoff = (int*)(ws + L.kvoff);
   hipLaunchKernelGGL(pg::plan_groups_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, cu_p, cu_s, gsz, c.ng, c.ns,
-                     c.tp, c.ts, pg::kFwdBM, pg::kKvBN, L.max_q, bwd ? L.max_kv : 0x7fffffffL, hdr, gi, qoff,
+                     c.tp, c.ts, pg::kFwdBM, pg::kKvBN, L.kv_chunks, L.max_q, bwd ? L.max_kv : 0x7fffffffL, hdr, gi, qoff,
                      kvoff);
   auto* qt = (pg::TileDesc*)(ws + L.qtiles);
   int* qo = (int*)(ws + L.qorder);
   if (L.max_q > 0) {
     const int blocks = (int)ceil_div_l(L.max_q, 256);
     hipLaunchKernelGGL(pg::plan_tiles_kernel, dim3(blocks), dim3(256), 0, st, cu_s, c.ng, pg::kFwdBM, pg::kKvBN,
-                       (int)L.max_q, hdr, gi, qoff, qt, 0);
+                       1, (int)L.max_q, hdr, gi, qoff, qt, 0);
     hipLaunchKernelGGL(pg::plan_rank_kernel, dim3(blocks), dim3(256), 0, st, hdr, qt, qo, 0);
   }
   if (bwd && L.max_kv > 0) {
@@ -170,7 +183,7 @@ int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p,
     int* ko = (int*)(ws + L.kvorder);
     const int blocks = (int)ceil_div_l(L.max_kv, 256);
     hipLaunchKernelGGL(pg::plan_tiles_kernel, dim3(blocks), dim3(256), 0, st, cu_s, c.ng, pg::kFwdBM, pg::kKvBN,
-                       (int)L.max_kv, hdr, gi, kvoff, kt, 1);
+                       L.kv_chunks, (int)L.max_kv, hdr, gi, kvoff, kt, 1);
     hipLaunchKernelGGL(pg::plan_rank_kernel, dim3(blocks), dim3(256), 0, st, hdr, kt, ko, 1);
   }
   if (c.ts > 0) {
@@ -208,6 +221,10 @@ void launch_bwd(const pg::BwdArgs& a, long max_q, long max_kv, hipStream_t st) {
     Timed tm(PG_K_DKDV, st);
     const long blocks = pg::xcd_grid_blocks(max_kv, a.h_kv, 1);
     hipLaunchKernelGGL((pg::dkdv_kernel<T, D>), dim3((unsigned)blocks), dim3(pg::kKvThreads), 0, st, a);
+    if (a.kv_chunks > 1 && a.total_prefix > 0) {
+      const long n = 2L * a.total_prefix * a.h_kv * D / 4;
+      hipLaunchKernelGGL((pg::kv_reduce_kernel<T, D>), dim3((unsigned)ceil_div_l(n, 256)), dim3(256), 0, st, a);
+    }
   }
   if (max_q > 0) {
     Timed tm(PG_K_DQ, st);
@@ -220,14 +237,20 @@ void launch_bwd(const pg::BwdArgs& a, long max_q, long max_kv, hipStream_t st) {
 
 extern "C" {
 
-size_t pg_attn_fwd_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q) {
-  if (n_groups < 0 || n_suffixes < 0 || total_prefix < 0 || total_suffix < 0 || h_q < 0) return 0;
-  return make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, false).total;
+size_t pg_attn_fwd_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q,
+                                  int h_kv, int head_dim) {
+  if (n_groups < 0 || n_suffixes < 0 || total_prefix < 0 || total_suffix < 0 || h_q < 0 || h_kv < 0 ||
+      head_dim < 0)
+    return 0;
+  return make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, false).total;
 }
 
-size_t pg_attn_bwd_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q) {
-  if (n_groups < 0 || n_suffixes < 0 || total_prefix < 0 || total_suffix < 0 || h_q < 0) return 0;
-  return make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, true).total;
+size_t pg_attn_bwd_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q,
+                                  int h_kv, int head_dim) {
+  if (n_groups < 0 || n_suffixes < 0 || total_prefix < 0 || total_suffix < 0 || h_q < 0 || h_kv < 0 ||
+      head_dim < 0)
+    return 0;
+  return make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, true).total;
 }
 
 const char* pg_status_string(int s) {
@@ -258,7 +281,7 @@ int pg_attn_fwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int t
     return fail(PG_EINVAL, "a prefix tensor pointer is NULL");
   if (total_suffix > 0 && (!q_suf || !k_suf || !v_suf || !o_suf || !lse_suf))
     return fail(PG_EINVAL, "a suffix tensor pointer is NULL");
-  const Layout L = make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, false);
+  const Layout L = make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, false);
   if (!workspace || workspace_bytes < L.total)
     return fail(PG_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
   if ((rc = device_ready())) return rc;
@@ -306,7 +329,7 @@ int pg_attn_bwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int t
   if (total_suffix > 0 && (!q_suf || !k_suf || !v_suf || !o_suf || !lse_suf || !do_suf || !dq_suf || !dk_suf ||
                            !dv_suf))
     return fail(PG_EINVAL, "a suffix tensor pointer is NULL");
-  const Layout L = make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, true);
+  const Layout L = make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, true);
   if (!workspace || workspace_bytes < L.total)
     return fail(PG_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
   if ((rc = device_ready())) return rc;
@@ -320,6 +343,8 @@ int pg_attn_bwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int t
   a.lse_pre = lse_pre; a.lse_suf = lse_suf;
   a.dq_pre = dq_pre; a.dk_pre = dk_pre; a.dv_pre = dv_pre; a.dq_suf = dq_suf; a.dk_suf = dk_suf; a.dv_suf = dv_suf;
   a.dsum = (float*)(ws + L.dsum);
+  a.part = (float*)(ws + L.part);
+  a.kv_chunks = L.kv_chunks;
   a.hdr = (const pg::PlanHeader*)(ws + L.hdr);
   a.ginfo = (const pg::GroupInfoEx*)(ws + L.ginfo);
   a.qtiles = (const pg::TileDesc*)(ws + L.qtiles);

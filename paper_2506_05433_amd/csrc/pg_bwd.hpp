@@ -27,6 +27,8 @@ struct BwdArgs {
   const float *lse_pre, *lse_suf;
   void *dq_pre, *dk_pre, *dv_pre, *dq_suf, *dk_suf, *dv_suf;
   float* dsum;  // [h_q][total_prefix + total_suffix]
+  float* part;  // [kv_chunks][2 (dK, dV)][total_prefix][h_kv][D] fp32 partials, when kv_chunks > 1
+  int kv_chunks;
   const PlanHeader* hdr;
   const GroupInfoEx* ginfo;
   const TileDesc *qtiles, *kvtiles;
@@ -144,7 +146,10 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
   const int nd = (rd_hi - rd_lo + BQ - 1) / BQ;
   const int nc = (rc_hi - rc_lo + BQ - 1) / BQ;
   const int per_head = nd + nc;
-  const int total = per_head * ratio;
+  // this workgroup's piece [it0, it1) of the walk (a prefix key tile may be split in chunks)
+  const int walk = per_head * ratio;
+  const int it0 = (int)((long)walk * td.chunk / td.nchunks);
+  const int it1 = (int)((long)walk * (td.chunk + 1) / td.nchunks);
   const float c = a.scale_log2;
 
   struct TileInfo {
@@ -184,7 +189,7 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
   fo.init(lane);
   float pf_lse = 0.f, pf_dsum = 0.f;
   int pf_seg = 0;
-  auto issue = [&](const TileInfo& ti, int it) {
+  auto issue = [&](const TileInfo& ti, int it) {  // `it` selects the buffer
     const T* Qs = (const T*)(ti.qsuf ? a.q_suf : a.q_pre);
     const T* Gs = (const T*)(ti.qsuf ? a.do_suf : a.do_pre);
     const size_t off = ((size_t)ti.q0 * a.h_q + ti.hq) * D;
@@ -206,18 +211,18 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     if (tid < BQ) { s_lse[buf][tid] = pf_lse; s_dsum[buf][tid] = pf_dsum; s_seg[buf][tid] = pf_seg; }
   };
 
-  TileInfo ti_cur = info(0, 0), ti_prev = ti_cur;  // tiles it and it - 1
-  int cur_hd = 0, cur_j = 0;
-  if (total > 0) { issue(ti_cur, 0); commit(0); }
+  int cur_hd = it0 / (per_head > 0 ? per_head : 1), cur_j = it0 - cur_hd * per_head;
+  TileInfo ti_cur = info(cur_hd, cur_j), ti_prev = ti_cur;  // tiles it and it - 1
+  if (it1 > it0) { issue(ti_cur, it0 % NBUF); commit(it0 % NBUF); }
   ldq.wait();
   __syncthreads();
 
-  for (int it = 0; it <= total; ++it) {
+  for (int it = it0; it <= it1; ++it) {
     int nxt_hd = cur_hd, nxt_j = cur_j + 1;
     if (nxt_j == per_head) { nxt_j = 0; ++nxt_hd; }
     const TileInfo ti_next = info(nxt_hd, nxt_j);
-    if (it + 1 < total) issue(ti_next, it + 1);
-    if (pwave && it < total && wave_active) {
+    if (it + 1 < it1) issue(ti_next, it + 1);
+    if (pwave && it < it1 && wave_active) {
       // ---------------- P-wave on tile it
       const int buf = it % NBUF;
       const TileInfo& ti = ti_cur;
@@ -271,7 +276,7 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
           }
         }
       }
-    } else if (!pwave && it > 0 && wave_active) {
+    } else if (!pwave && it > it0 && wave_active) {
       // ---------------- G-wave on tile it-1
       const int buf = (it - 1) % NBUF;
       const TileInfo& ti = ti_prev;
@@ -307,7 +312,7 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
         }
       }
     }
-    if (it + 1 < total) commit((it + 1) % NBUF);
+    if (it + 1 < it1) commit((it + 1) % NBUF);
     ti_prev = ti_cur;
     ti_cur = ti_next;
     cur_hd = nxt_hd;
@@ -317,9 +322,23 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
   }
 
   if (!wave_active || !kvalid) return;
+  const float sc = pwave ? 1.f : a.scale;
+  if (td.nchunks > 1) {
+    // fp32 partial of this chunk; kv_reduce_kernel adds the chunks in order
+    float* out = a.part + (((size_t)td.chunk * 2 + (pwave ? 1 : 0)) * a.total_prefix + key) * a.h_kv * D +
+                 (size_t)kvh * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d0 = 32 * db + 8 * i + 4 * hh;
+        *(f32x4*)(out + d0) = f32x4{acc[db][4 * i] * sc, acc[db][4 * i + 1] * sc, acc[db][4 * i + 2] * sc,
+                                    acc[db][4 * i + 3] * sc};
+      }
+    return;
+  }
   T* out = (T*)(pwave ? (kv_suffix ? a.dv_suf : a.dv_pre) : (kv_suffix ? a.dk_suf : a.dk_pre)) +
            ((size_t)key * a.h_kv + kvh) * D;
-  const float sc = pwave ? 1.f : a.scale;
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -328,6 +347,22 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
       E::store4(out + d0, acc[db][4 * i] * sc, acc[db][4 * i + 1] * sc, acc[db][4 * i + 2] * sc,
                 acc[db][4 * i + 3] * sc);
     }
+}
+
+// dK_pre, dV_pre = sum over the kv_chunks partials, in chunk order (deterministic).
+template <typename T, int D>
+__global__ void __launch_bounds__(256) kv_reduce_kernel(const BwdArgs a) {
+  const long n4 = (long)a.total_prefix * a.h_kv * D / 4;  // float4 groups per tensor
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= 2 * n4) return;
+  const int which = i >= n4;  // 0: dK, 1: dV
+  const long e = i - which * n4;
+  const size_t stride = (size_t)2 * a.total_prefix * a.h_kv * D;  // floats per chunk
+  const float* src = a.part + (size_t)which * a.total_prefix * a.h_kv * D + 4 * e;
+  f32x4 s = *(const f32x4*)src;
+  for (int c = 1; c < a.kv_chunks; ++c) s += *(const f32x4*)(src + c * stride);
+  T* dst = (T*)(which ? a.dv_pre : a.dk_pre) + 4 * e;
+  Elt<T>::store4(dst, s[0], s[1], s[2], s[3]);
 }
 
 // ------------------------------------------------------------------ dQ (query-stationary)

@@ -35,7 +35,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 //  kv tiles: kind 0 = prefix keys [row0,row1); kind 1 = response keys [row0,row1);
 //            aux = end of the response rows that can see them (end of the member owning row1-1).
 struct TileDesc {
-  int kind, group, row0, row1, aux, work, pad0, pad1;
+  int kind, group, row0, row1, aux, work, chunk, nchunks;
 };
 
 // Per-group ranges: prefix rows [p0,p1), response rows [s0,s1).

@@ -57,7 +57,7 @@ constexpr int kPlanThreads = 1024;
 // One block. Validates and computes per-group ranges and tile offsets.
 __global__ void __launch_bounds__(kPlanThreads) plan_groups_kernel(
     const int* __restrict__ cu_p, const int* __restrict__ cu_s, const int* __restrict__ gsz,
-    int ng, int ns, int tp, int ts, int bm, int bkv, long max_q, long max_kv,
+    int ng, int ns, int tp, int ts, int bm, int bkv, int kv_chunks, long max_q, long max_kv,
     PlanHeader* hdr, GroupInfoEx* ginfo, int* qoff, int* kvoff) {
   __shared__ int tmp[kPlanThreads];
   __shared__ int err;
@@ -104,7 +104,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_groups_kernel(
       gi.pad0 = gi.pad1 = 0;
       ginfo[g] = gi;
       nq = ceil_div(gi.p1 - gi.p0, bm) + ceil_div(gi.s1 - gi.s0, bm);
-      nkv = ceil_div(gi.p1 - gi.p0, bkv) + ceil_div(gi.s1 - gi.s0, bkv);
+      nkv = ceil_div(gi.p1 - gi.p0, bkv) * kv_chunks + ceil_div(gi.s1 - gi.s0, bkv);
     }
     const int iq = block_inclusive_scan<kPlanThreads>(nq, tmp);
     const int ikv = block_inclusive_scan<kPlanThreads>(nkv, tmp);
@@ -128,7 +128,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_groups_kernel(
 }
 
 // One thread per (possible) tile: fills the descriptors. `which` 0 = query tiles, 1 = kv tiles.
-__global__ void plan_tiles_kernel(const int* __restrict__ cu_s, int ng, int bm, int bkv, int max_tiles,
+__global__ void plan_tiles_kernel(const int* __restrict__ cu_s, int ng, int bm, int bkv, int kv_chunks, int max_tiles,
                                   const PlanHeader* hdr, const GroupInfoEx* __restrict__ ginfo,
                                   const int* __restrict__ off, TileDesc* tiles, int which) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -138,13 +138,18 @@ __global__ void plan_tiles_kernel(const int* __restrict__ cu_s, int ng, int bm, 
   // skip groups with zero tiles that share the offset of the next one
   const GroupInfoEx gi = ginfo[g];
   const int b = which ? bkv : bm;
-  const int local = i - off[g];
-  const int np = ceil_div(gi.p1 - gi.p0, b);
+  const int chunks = which ? kv_chunks : 1;
+  int local = i - off[g];
+  const int np = ceil_div(gi.p1 - gi.p0, b) * chunks;
   TileDesc d;
   d.group = g;
-  d.pad0 = d.pad1 = 0;
+  d.chunk = 0;
+  d.nchunks = 1;
   if (local < np) {
     d.kind = 0;
+    d.chunk = local % chunks;
+    d.nchunks = chunks;
+    local /= chunks;
     d.row0 = gi.p0 + local * b;
     d.row1 = min(d.row0 + b, gi.p1);
     if (!which) {
@@ -152,7 +157,7 @@ __global__ void plan_tiles_kernel(const int* __restrict__ cu_s, int ng, int bm, 
       d.work = d.row1 - gi.p0;                          // keys seen by the last row
     } else {
       d.aux = 0;
-      d.work = (gi.p1 - d.row0) + (gi.s1 - gi.s0);      // query rows that see these keys
+      d.work = ((gi.p1 - d.row0) + (gi.s1 - gi.s0)) / chunks;  // query rows that see these keys
     }
   } else {
     d.kind = 1;

@@ -36,13 +36,13 @@ def test_status_strings():
 
 
 def test_workspace_sizes_grow_with_the_problem():
-    f1 = binding.workspace_bytes("fwd", 1, 8, 4096, 5120, 32)
-    b1 = binding.workspace_bytes("bwd", 1, 8, 4096, 5120, 32)
-    f2 = binding.workspace_bytes("fwd", 8, 128, 73275, 266240, 64)
+    f1 = binding.workspace_bytes("fwd", 1, 8, 4096, 5120, 32, 8, 128)
+    b1 = binding.workspace_bytes("bwd", 1, 8, 4096, 5120, 32, 8, 128)
+    f2 = binding.workspace_bytes("fwd", 8, 128, 73275, 266240, 64, 8, 128)
     assert 0 < f1 < b1 and f1 < f2
     # the backward workspace holds rowsum(dO*O): h_q * rows floats
     assert b1 >= 32 * (4096 + 5120) * 4
-    assert binding.workspace_bytes("fwd", -1, 0, 0, 0, 1) == 0
+    assert binding.workspace_bytes("fwd", -1, 0, 0, 0, 1, 1, 64) == 0
 
 
 def _call_fwd(**over):
