@@ -30,7 +30,9 @@
  *                                  members of group g follow those of group g-1.
  * Empty prefixes, empty responses and groups without members are legal.
  * GQA: query head h reads key/value head h / (h_q / h_kv); h_q % h_kv == 0.
- * head_dim must be 64 or 128. softmax_scale multiplies q.k before the softmax
+ * head_dim must be 64 or 128 and h_q * head_dim at most 65536 (else
+ * PG_EUNSUPPORTED); (total_prefix + total_suffix) * h_q must fit in 31 bits.
+ * softmax_scale multiplies q.k before the softmax
  * (q and k arrive already rotary-encoded, as Algorithm 1 requires).
  *
  * Ownership and execution: every pointer except those of the size queries is
@@ -63,7 +65,7 @@ typedef enum { PG_BF16 = 0, PG_FP32 = 1 } pg_dtype;
 typedef enum {
   PG_OK = 0,
   PG_EINVAL = 1,       /* bad argument (sizes, null pointers, scale, grouping arrays) */
-  PG_EUNSUPPORTED = 2, /* valid but unsupported (head_dim, dtype)                      */
+  PG_EUNSUPPORTED = 2, /* valid but unsupported (head_dim, dtype, size limits)         */
   PG_EWORKSPACE = 3,   /* workspace missing or smaller than the size query returns     */
   PG_EHIP = 4          /* HIP runtime failure (no device, launch error, ...)           */
 } pg_status;

@@ -133,6 +133,8 @@ int check_common(const Common& c, const int32_t* cu_p, const int32_t* cu_s, cons
   if (c.h_q <= 0 || c.h_kv <= 0 || c.h_q % c.h_kv != 0)
     return fail(PG_EINVAL, "h_q=%d must be a positive multiple of h_kv=%d", c.h_q, c.h_kv);
   if (c.d != 64 && c.d != 128) return fail(PG_EUNSUPPORTED, "head_dim=%d (supported: 64, 128)", c.d);
+  // a staged tile's byte range (at most 128 rows of h * head_dim fp32) must stay below 2^31
+  if ((long)c.h_q * c.d > 65536) return fail(PG_EUNSUPPORTED, "h_q*head_dim=%ld exceeds 65536", (long)c.h_q * c.d);
   if (!(std::isfinite(c.scale) && c.scale > 0.f)) return fail(PG_EINVAL, "softmax_scale must be finite and > 0");
   const long rows = (long)c.tp + c.ts;
   if (rows * c.h_q > 0x7fffffffL || (long)c.tp * c.h_q * c.d > (1L << 40))

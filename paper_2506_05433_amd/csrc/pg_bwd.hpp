@@ -211,21 +211,37 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     if (tid < BQ) { s_lse[buf][tid] = pf_lse; s_dsum[buf][tid] = pf_dsum; s_seg[buf][tid] = pf_seg; }
   };
 
-  int cur_hd = it0 / (per_head > 0 ? per_head : 1), cur_j = it0 - cur_hd * per_head;
-  TileInfo ti_cur = info(cur_hd, cur_j), ti_prev = ti_cur;  // tiles it and it - 1
-  if (it1 > it0) { issue(ti_cur, it0 % NBUF); commit(it0 % NBUF); }
-  ldq.wait();
-  __syncthreads();
+  // The walk: every wave stages its share of tile it+1, works on its tile, and meets the
+  // others at one barrier per tile. The two roles run this skeleton as separate loops
+  // (`work` is the role's body), so each keeps its accumulator in place; both loops
+  // execute the same barriers, and the role is uniform per wave.
+  auto walk_tiles = [&](auto&& work) {
+    int cur_hd = it0 / (per_head > 0 ? per_head : 1), cur_j = it0 - cur_hd * per_head;
+    TileInfo ti_cur = info(cur_hd, cur_j), ti_prev = ti_cur;  // tiles it and it - 1
+    if (it1 > it0) { issue(ti_cur, it0 % NBUF); commit(it0 % NBUF); }
+    ldq.wait();
+    __syncthreads();
+    for (int it = it0; it <= it1; ++it) {
+      int nxt_hd = cur_hd, nxt_j = cur_j + 1;
+      if (nxt_j == per_head) { nxt_j = 0; ++nxt_hd; }
+      const TileInfo ti_next = info(nxt_hd, nxt_j);
+      if (it + 1 < it1) issue(ti_next, it + 1);
+      work(it, ti_cur, ti_prev);
+      if (it + 1 < it1) commit((it + 1) % NBUF);
+      ti_prev = ti_cur;
+      ti_cur = ti_next;
+      cur_hd = nxt_hd;
+      cur_j = nxt_j;
+      ldq.wait();
+      __syncthreads();
+    }
+  };
 
-  for (int it = it0; it <= it1; ++it) {
-    int nxt_hd = cur_hd, nxt_j = cur_j + 1;
-    if (nxt_j == per_head) { nxt_j = 0; ++nxt_hd; }
-    const TileInfo ti_next = info(nxt_hd, nxt_j);
-    if (it + 1 < it1) issue(ti_next, it + 1);
-    if (pwave && it < it1 && wave_active) {
+  if (pwave) {
+    walk_tiles([&](int it, const TileInfo& ti, const TileInfo&) {
+      if (!(it < it1 && wave_active)) return;
       // ---------------- P-wave on tile it
       const int buf = it % NBUF;
-      const TileInfo& ti = ti_cur;
       bool skip, full;
       visibility(ti, buf, skip, full);
       if (!skip) {
@@ -276,10 +292,12 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
           }
         }
       }
-    } else if (!pwave && it > it0 && wave_active) {
+    });
+  } else {
+    walk_tiles([&](int it, const TileInfo&, const TileInfo& ti) {
+      if (!(it > it0 && wave_active)) return;
       // ---------------- G-wave on tile it-1
       const int buf = (it - 1) % NBUF;
-      const TileInfo& ti = ti_prev;
       bool skip, full;
       visibility(ti, buf, skip, full);
       if (!skip) {
@@ -311,14 +329,7 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
           }
         }
       }
-    }
-    if (it + 1 < it1) commit((it + 1) % NBUF);
-    ti_prev = ti_cur;
-    ti_cur = ti_next;
-    cur_hd = nxt_hd;
-    cur_j = nxt_j;
-    ldq.wait();
-    __syncthreads();
+    });
   }
 
   if (!wave_active || !kvalid) return;

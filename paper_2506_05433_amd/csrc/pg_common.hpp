@@ -275,6 +275,17 @@ struct Elt<float> {
 // as zeros with no per-row test. Thread tid owns 16-byte chunk tid % C of rows
 // tid / C + i * (NT / C); its global and LDS offsets are affine in i (the swizzle
 // repeats every 16 rows), so they are computed once.
+// Byte range of a tile's buffer resource: only the rows the tile holds (at most `rows`)
+// count, so the range stays far below 2^31 whatever the length of the sequence behind
+// them; the host bounds h * head_dim so that rows * row_bytes does too. Reads past the
+// range return zeros, which is how ragged tiles and padding lanes are filled. The value is
+// uniform at every call site; readfirstlane keeps it in a scalar register (a per-lane value
+// would make the compiler wrap each buffer load in a loop over distinct descriptors).
+__device__ __forceinline__ int range_bytes(int valid_rows, int rows, int row_bytes) {
+  const int r = valid_rows < rows ? (valid_rows > 0 ? valid_rows : 0) : rows;
+  return __builtin_amdgcn_readfirstlane(r * row_bytes);
+}
+
 template <typename T, int ROWS, int D, int NT>
 struct TileLoader {
   static constexpr int kChunks = D * (int)sizeof(T) / 16;  // 16-byte chunks per row
@@ -297,7 +308,7 @@ struct TileLoader {
     loff = LdsTile<T, D>::chunk_off(r, k);
   }
   __device__ __forceinline__ void load(char* /*lds*/, const T* base, int gstride, int valid_rows) {
-    const int bytes = valid_rows * gstride * (int)sizeof(T);
+    const int bytes = range_bytes(valid_rows, ROWS, gstride * (int)sizeof(T));
     __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, bytes, 0x00020000);
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
@@ -350,7 +361,7 @@ struct DirectLoader {
     }
   }
   __device__ __forceinline__ void load(char* lds, const bf16* base, int gstride, int valid_rows) {
-    const int bytes = valid_rows * gstride * 2;
+    const int bytes = range_bytes(valid_rows, ROWS, gstride * 2);
     __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, bytes, 0x00020000);
 #pragma unroll
     for (int k = 0; k < kPerWave; ++k) {

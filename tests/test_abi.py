@@ -59,6 +59,7 @@ def _call_fwd(**over):
 @pytest.mark.parametrize("over,status", [
     (dict(dtype=7), 2),
     (dict(d=96), 2),
+    (dict(h_q=1024, h_kv=2), 2),
     (dict(h_q=6, h_kv=4), 1),
     (dict(h_kv=0), 1),
     (dict(scale=float("nan")), 1),

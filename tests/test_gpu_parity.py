@@ -224,3 +224,42 @@ def test_invalid_grouping_arrays_do_no_work(monkeypatch):
         binding.fwd(dev["q_pre"], dev["k_pre"], dev["v_pre"], dev["q_suf"], dev["k_suf"], dev["v_suf"],
                     dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], dev["scale"])
     assert e.value.status == 1
+
+
+def test_dense_query_range_of_two_gib():
+    """A prefix key tile whose dense query range (every response row of the group) spans 2^31 bytes.
+
+    16 members of 1024 rows and h_q * head_dim = 65536 give 16384 rows of 128 KiB: the byte range
+    of the staged query tiles must be that of the tile, not of the whole remaining range. Checked on
+    sampled rows and keys against the oracle, and on sum dV = sum dO and sum dK = 0 over every key
+    of kv head 0 (the softmax rows sum to one; each row of dS sums to zero).
+    """
+    prob = make_problem("single_group", seed=3, lengths=([128], [16], [1024] * 16), h_q=512, h_kv=64)
+    print(f"[parity] dense 2 GiB range: total_prefix={prob.total_prefix} total_suffix={prob.total_suffix} "
+          f"h_q={prob.h_q} h_kv={prob.h_kv}", flush=True)
+    binding = _dev()
+    dev = binding.to_device(prob, "cuda")
+    f = binding.run_fwd(dev)
+    g = binding.run_bwd(dev, f)
+    torch.cuda.synchronize()
+    out = dict(zip(OUTS, f))
+    out.update(zip(GRADS, g))
+    t = host_view(prob)
+    heads = [0, 7, 300, 511]
+    rows = [0, 1023, 1024, 8191, 16383]
+    r = query_rows(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, "suf", rows, heads)
+    idx_r, idx_h = torch.tensor(rows, device="cuda"), torch.tensor(heads, device="cuda")
+    check("o_suf", to_host(out["o_suf"][idx_r][:, idx_h]), r["o"], prob.dtype)
+    check("dq_suf", to_host(out["dq_suf"][idx_r][:, idx_h]), r["dq"], prob.dtype)
+    keys = [0, 64, 127]
+    r = key_gradients(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, 0, 0, "pre", keys)
+    check("dk_pre", to_host(out["dk_pre"][keys, 0]), r["dk"], prob.dtype)
+    check("dv_pre", to_host(out["dv_pre"][keys, 0]), r["dv"], prob.dtype)
+    ratio = prob.h_q // prob.h_kv
+    dv_sum = out["dv_pre"][:, 0].double().sum(0) + out["dv_suf"][:, 0].double().sum(0)
+    do_sum = dev["do_pre"][:, :ratio].double().sum((0, 1)) + dev["do_suf"][:, :ratio].double().sum((0, 1))
+    rel = float((dv_sum - do_sum).abs().max() / do_sum.abs().max())
+    dk = torch.cat([out["dk_pre"][:, 0], out["dk_suf"][:, 0]]).double()
+    rel_k = float(dk.sum(0).abs().max() / dk.abs().sum(0).max())
+    print(f"sum dV vs sum dO rel={rel:.3e}; |sum dK| / sum |dK| = {rel_k:.3e}", flush=True)
+    assert rel < 3e-2 and rel_k < 1e-2
