@@ -10,6 +10,10 @@ Repeated-Prefix Forward of Section 2.1, Eq. (1): each group member's sequence
 Eq. (3). Lemma 1 (Section 2.2, proof in Appendix A.1) states that the
 Shared-Prefix Forward gives the same outputs and gradients, so the repeated
 computation is the reference the grouped kernels are checked against.
+
+``rope`` is the step before the attention (Algorithm 1 takes rotary-encoded q
+and k): the rotary embedding with the repeated-layout position ids that the
+grouped layout keeps.
 """
 from .attention import (  # noqa: F401
     causal_attention,
@@ -17,3 +21,4 @@ from .attention import (  # noqa: F401
     key_gradients,
     query_rows,
 )
+from .rope import grouped_positions, inv_freq, pair_index, rope  # noqa: F401,E402
