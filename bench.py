@@ -93,6 +93,35 @@ def alloc(binding, torch, dev, prob):
     return bufs
 
 
+def time_rope(binding, torch, dev, prob, steps, warmup):
+    """The grouped-position rotary embedding of q and k (both sides) on this workload, out of place.
+
+    HBM-bound: every element of q and k is read once and written once, so the algorithmic traffic of one
+    launch is 2 * (total_prefix + total_suffix) * (h_q + h_kv) * head_dim * element bytes; the HBM peak is
+    8 TB/s.
+    """
+    ins = (dev["q_pre"], dev["q_suf"], dev["k_pre"], dev["k_suf"])
+    outs = tuple(torch.empty_like(t) for t in ins)
+    ws = torch.empty(int(binding.lib().pg_rope_workspace_size(len(prob.prefix_lens))), device="cuda",
+                     dtype=torch.uint8)
+    grp = (dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"])
+    for _ in range(warmup):
+        binding.rope(*ins, *grp, out=outs, workspace=ws)
+    torch.cuda.synchronize()
+    binding.timing_start()
+    for _ in range(steps):
+        binding.rope(*ins, *grp, out=outs, workspace=ws)
+    torch.cuda.synchronize()
+    binding.timing_stop()
+    n, tot = binding.timing_get("rope")
+    ms = tot / n
+    el = 2 if prob.dtype == "bf16" else 4
+    nbytes = 2 * (prob.total_prefix + prob.total_suffix) * (prob.h_q + prob.h_kv) * prob.head_dim * el
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"kernel": "rope", "ms": round(ms, 4), "bytes": nbytes, "achieved_GBps": round(gbs, 1),
+            "peak_GBps": 8000.0, "frac": round(gbs / 8000.0, 4), "bound": "hbm"}
+
+
 def cpu_baseline(prob, useful_per_pair_head, budget_s):
     """The oracle (fp64 numpy, as it stands) on a bounded sample of the workload.
 
@@ -223,6 +252,7 @@ def main():
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
                      "traffic": recorded_traffic(dom, wl.name), "source_sha": kernel_source_sha()},
     }
+    out["rope"] = time_rope(binding, torch, dev, prob, args.steps, args.warmup)
     if not args.no_repeated:
         rep = repeated_layout(prob)
         del dev, bufs

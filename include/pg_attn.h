@@ -116,6 +116,54 @@ int pg_attn_bwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int t
                 void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Rotary position embedding with grouped position ids, the step before the
+ * attention calls (Algorithm 1 takes q and k already rotary-encoded). Each
+ * token gets the position it has in the Repeated-Prefix Forward (Section 2,
+ * "Algorithm implementation", after Eq. (4)): prefix row t of a group is at
+ * position t, row j of any member's response at P + j, P being the group's
+ * prefix length. Positions are derived from the grouping arrays (same
+ * meaning as for pg_attn_fwd); no position tensor is needed.
+ *
+ * The first rotary_dim dimensions of every head vector form rotary_dim / 2
+ * pairs; pair i turns by the angle pos * base^(-2 i / rotary_dim) (computed in
+ * double precision), the other dimensions are copied unchanged. Pair layout:
+ * half-split (pair i = dims i and i + rotary_dim/2) by default,
+ * PG_ROPE_INTERLEAVED for dims 2i and 2i+1. PG_ROPE_INVERSE turns by the
+ * negative angle: applied to the gradients of the rotated q and k it gives the
+ * gradients of the unrotated ones (the rotation is orthogonal).
+ *
+ * Tensors: q_* [rows, h_q, head_dim], k_* [rows, h_kv, head_dim], dtype as for
+ * the attention calls, contiguous, 16-byte aligned device pointers; *_out may
+ * equal the input (in place). h_q or h_kv may be 0 to rotate only the other
+ * tensor (its pointers may then be NULL). head_dim is 64 or 128, rotary_dim a
+ * multiple of 16 in [16, head_dim], (h_q + h_kv) * head_dim <= 65536, base
+ * finite and > 0. Workspace: pg_rope_workspace_size(n_groups) bytes of device
+ * memory. Errors as for the attention calls (host checks before any launch;
+ * inconsistent grouping arrays leave the outputs untouched, reported only
+ * under PG_DEBUG_VALIDATE=1).
+ */
+typedef enum { PG_ROPE_INVERSE = 1, PG_ROPE_INTERLEAVED = 2 } pg_rope_flags;
+
+size_t pg_rope_workspace_size(int n_groups);
+
+int pg_rope(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+            const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+            int h_q, int h_kv, int head_dim, int rotary_dim, double base, int flags,
+            const void* q_pre, const void* q_suf, const void* k_pre, const void* k_suf,
+            void* q_pre_out, void* q_suf_out, void* k_pre_out, void* k_suf_out,
+            void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The grouped position ids themselves: pos_pre [total_prefix] and pos_suf
+ * [total_suffix] int32 device arrays, by the rule of pg_rope (for callers that
+ * apply their own positional encoding). Workspace as for pg_rope.
+ */
+int pg_grouped_positions(int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                         const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                         int32_t* pos_pre, int32_t* pos_suf, void* workspace, size_t workspace_bytes,
+                         void* stream);
+
+/*
  * Kernel timing for benchmarks. Between pg_timing_start() and pg_timing_stop()
  * every call brackets each of its kernel launches with a pair of HIP events
  * recorded on the call's stream (at most 16384 launches are recorded per start;
@@ -129,7 +177,8 @@ typedef enum {
   PG_K_FWD = 1,      /* forward attention kernel                              */
   PG_K_BWD_DOT = 2,  /* backward: rowsum(dO * O)                              */
   PG_K_DKDV = 3,     /* backward: dK, dV (key-stationary, G-way prefix sum)   */
-  PG_K_DQ = 4        /* backward: dQ (query-stationary)                       */
+  PG_K_DQ = 4,       /* backward: dQ (query-stationary)                       */
+  PG_K_ROPE = 5      /* rotary embedding kernel of pg_rope                    */
 } pg_kernel;
 
 int pg_timing_start(void);

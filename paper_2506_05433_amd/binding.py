@@ -26,6 +26,9 @@ SIGNATURES = {
     "pg_attn_bwd_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
     "pg_attn_fwd": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 10 + [_P, _Z, _P]),
     "pg_attn_bwd": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 18 + [_P, _Z, _P]),
+    "pg_rope_workspace_size": (_Z, [_I]),
+    "pg_rope": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _I, ctypes.c_double, _I] + [_P] * 8 + [_P, _Z, _P]),
+    "pg_grouped_positions": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _Z, _P]),
     "pg_timing_start": (_I, []),
     "pg_timing_stop": (_I, []),
     "pg_timing_get": (_I, [_I, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)]),
@@ -55,7 +58,8 @@ def lib():
     return _lib
 
 
-KERNELS = {"plan": 0, "fwd": 1, "bwd_dot": 2, "dkdv": 3, "dq": 4}
+KERNELS = {"plan": 0, "fwd": 1, "bwd_dot": 2, "dkdv": 3, "dq": 4, "rope": 5}
+ROPE_INVERSE, ROPE_INTERLEAVED = 1, 2
 
 
 def timing_start():
@@ -155,6 +159,49 @@ def bwd(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, o_pre, o_suf, lse_pre, lse_suf
         _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(torch, dev))
     _check(st)
     return out
+
+
+def rope(q_pre, q_suf, k_pre, k_suf, cu_prefix, cu_suffix, group_sizes, base=10000.0, rotary_dim=None,
+         inverse=False, interleaved=False, out=None, workspace=None):
+    """Rotary embedding with grouped positions (pg_rope). q_* [rows, h_q, d], k_* [rows, h_kv, d]; either
+    pair may be None to rotate only the other. ``out`` = (q_pre, q_suf, k_pre, k_suf) destinations (may be
+    the inputs themselves); new tensors by default. Returns the four outputs (None where not rotated)."""
+    import torch
+    ref = q_pre if q_pre is not None else k_pre
+    ng, ns = group_sizes.numel(), cu_suffix.numel() - 1
+    tp = ref.shape[0]
+    ts = (q_suf if q_suf is not None else k_suf).shape[0]
+    d = ref.shape[2]
+    hq = q_pre.shape[1] if q_pre is not None else 0
+    hkv = k_pre.shape[1] if k_pre is not None else 0
+    ins = (q_pre, q_suf, k_pre, k_suf)
+    if out is None:
+        out = tuple(None if t is None else torch.empty_like(t) for t in ins)
+    if workspace is None:
+        workspace = torch.empty(int(lib().pg_rope_workspace_size(ng)), device=ref.device, dtype=torch.uint8)
+    flags = (ROPE_INVERSE if inverse else 0) | (ROPE_INTERLEAVED if interleaved else 0)
+    st = lib().pg_rope(_dtype_code(torch, ref.dtype), ng, ns, tp, ts, _ptr(cu_prefix), _ptr(cu_suffix),
+                       _ptr(group_sizes), hq, hkv, d, d if rotary_dim is None else int(rotary_dim), float(base),
+                       flags, *[_ptr(t) for t in ins], *[_ptr(t) for t in out],
+                       _ptr(workspace), workspace.numel(), _stream(torch, ref.device))
+    _check(st)
+    return out
+
+
+def grouped_positions(total_prefix, total_suffix, cu_prefix, cu_suffix, group_sizes, workspace=None):
+    """(pos_pre, pos_suf) int32 device tensors of the grouped position ids (pg_grouped_positions)."""
+    import torch
+    dev = cu_suffix.device
+    ng, ns = group_sizes.numel(), cu_suffix.numel() - 1
+    pos_pre = torch.empty(total_prefix, device=dev, dtype=torch.int32)
+    pos_suf = torch.empty(total_suffix, device=dev, dtype=torch.int32)
+    if workspace is None:
+        workspace = torch.empty(int(lib().pg_rope_workspace_size(ng)), device=dev, dtype=torch.uint8)
+    st = lib().pg_grouped_positions(ng, ns, total_prefix, total_suffix, _ptr(cu_prefix), _ptr(cu_suffix),
+                                    _ptr(group_sizes), _ptr(pos_pre), _ptr(pos_suf), _ptr(workspace),
+                                    workspace.numel(), _stream(torch, dev))
+    _check(st)
+    return pos_pre, pos_suf
 
 
 def to_device(prob, device="cuda"):

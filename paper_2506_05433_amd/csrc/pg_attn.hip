@@ -15,6 +15,7 @@
 #include "pg_bwd.hpp"
 #include "pg_fwd.hpp"
 #include "pg_plan.hpp"
+#include "pg_rope.hpp"
 
 namespace {
 
@@ -235,6 +236,58 @@ void launch_bwd(const pg::BwdArgs& a, long max_q, long max_kv, hipStream_t st) {
   }
 }
 
+
+// ---------------------------------------------------------------- rotary embedding
+// Workspace of the rope / positions calls: the planner's header and per-group ranges.
+struct RopeLayout {
+  size_t hdr, ginfo, qoff, kvoff, total;
+};
+
+RopeLayout rope_layout(int ng) {
+  RopeLayout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
+  L.hdr = take(sizeof(pg::PlanHeader));
+  L.ginfo = take(sizeof(pg::GroupInfoEx) * (size_t)(ng > 0 ? ng : 1));
+  L.qoff = take(sizeof(int) * (size_t)(ng + 1));
+  L.kvoff = take(sizeof(int) * (size_t)(ng + 1));
+  L.total = off;
+  return L;
+}
+
+int check_grouping(int ng, int ns, int tp, int ts, const int32_t* cu_p, const int32_t* cu_s, const int32_t* gsz) {
+  if (ng < 0 || ns < 0 || tp < 0 || ts < 0)
+    return fail(PG_EINVAL, "negative size (n_groups=%d n_suffixes=%d total_prefix=%d total_suffix=%d)", ng, ns,
+                tp, ts);
+  if (ng == 0 && (tp != 0 || ns != 0)) return fail(PG_EINVAL, "no groups but nonzero prefix rows or members");
+  if (ns == 0 && ts != 0) return fail(PG_EINVAL, "no members but nonzero total_suffix");
+  if ((long)tp + ts > 0x7fffffffL) return fail(PG_EUNSUPPORTED, "more than 2^31-1 rows");
+  if (ng > 0 && (!cu_p || !gsz || !cu_s)) return fail(PG_EINVAL, "a grouping array is NULL");
+  return PG_OK;
+}
+
+// Validates the grouping arrays on the device and fills the per-group ranges the row ->
+// position mapping reads (the first planner kernel of the attention calls).
+int launch_rope_plan(const RopeLayout& L, char* ws, int ng, int ns, int tp, int ts, const int32_t* cu_p,
+                     const int32_t* cu_s, const int32_t* gsz, hipStream_t st) {
+  auto* hdr = (pg::PlanHeader*)(ws + L.hdr);
+  hipLaunchKernelGGL(pg::plan_groups_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, cu_p, cu_s, gsz, ng, ns, tp,
+                     ts, pg::kFwdBM, pg::kKvBN, 1, 0x7fffffffL, 0x7fffffffL, hdr, (pg::GroupInfoEx*)(ws + L.ginfo),
+                     (int*)(ws + L.qoff), (int*)(ws + L.kvoff));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "planner launch");
+  if (debug_validate()) {
+    pg::PlanHeader h;
+    e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "PG_DEBUG_VALIDATE readback");
+    if (h.error) return fail(PG_EINVAL, "grouping arrays are inconsistent (checked on the device)");
+  }
+  return PG_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
 }  // namespace
 
 extern "C" {
@@ -399,6 +452,106 @@ int pg_timing_get(int kernel, int* launches, double* total_ms) {
   }
   *launches = cnt;
   *total_ms = tot;
+  return PG_OK;
+}
+
+size_t pg_rope_workspace_size(int n_groups) {
+  if (n_groups < 0) return 0;
+  return rope_layout(n_groups).total;
+}
+
+int pg_rope(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+            const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+            int h_q, int h_kv, int head_dim, int rotary_dim, double base, int flags,
+            const void* q_pre, const void* q_suf, const void* k_pre, const void* k_suf,
+            void* q_pre_out, void* q_suf_out, void* k_pre_out, void* k_suf_out,
+            void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  int rc = check_grouping(n_groups, n_suffixes, total_prefix, total_suffix, cu_prefix_lens, cu_suffix_lens,
+                          group_sizes);
+  if (rc) return rc;
+  if (dtype != PG_BF16 && dtype != PG_FP32) return fail(PG_EUNSUPPORTED, "dtype %d is not PG_BF16 or PG_FP32", dtype);
+  if (head_dim != 64 && head_dim != 128) return fail(PG_EUNSUPPORTED, "head_dim=%d (supported: 64, 128)", head_dim);
+  if (h_q < 0 || h_kv < 0 || h_q + h_kv == 0) return fail(PG_EINVAL, "h_q=%d h_kv=%d: need h_q + h_kv > 0", h_q, h_kv);
+  if ((long)(h_q + h_kv) * head_dim > 65536)
+    return fail(PG_EUNSUPPORTED, "(h_q + h_kv) * head_dim exceeds 65536");
+  if (rotary_dim < 16 || rotary_dim > head_dim || rotary_dim % 16 != 0)
+    return fail(PG_EUNSUPPORTED, "rotary_dim=%d (a multiple of 16 in [16, head_dim=%d])", rotary_dim, head_dim);
+  if (!(std::isfinite(base) && base > 0.0)) return fail(PG_EINVAL, "base must be finite and > 0");
+  if (flags & ~(PG_ROPE_INVERSE | PG_ROPE_INTERLEAVED)) return fail(PG_EINVAL, "unknown flags 0x%x", flags);
+  const void* ins[4] = {q_pre, q_suf, k_pre, k_suf};
+  void* outs[4] = {q_pre_out, q_suf_out, k_pre_out, k_suf_out};
+  for (int t = 0; t < 4; ++t) {
+    const bool used = (t < 2 ? h_q : h_kv) > 0 && (t % 2 == 0 ? total_prefix : total_suffix) > 0;
+    if (!used) continue;
+    if (!ins[t] || !outs[t]) return fail(PG_EINVAL, "a tensor pointer is NULL");
+    if (!aligned16(ins[t]) || !aligned16(outs[t])) return fail(PG_EINVAL, "tensor pointers must be 16-byte aligned");
+  }
+  const RopeLayout L = rope_layout(n_groups);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(PG_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
+  if ((rc = device_ready())) return rc;
+  const int rows = total_prefix + total_suffix;
+  if (rows == 0) return PG_OK;
+  hipStream_t st = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  pg::RopeArgs a{};
+  a.cu_p = cu_prefix_lens; a.cu_s = cu_suffix_lens;
+  a.hdr = (const pg::PlanHeader*)(ws + L.hdr);
+  a.ginfo = (const pg::GroupInfoEx*)(ws + L.ginfo);
+  a.ng = n_groups; a.ns = n_suffixes; a.tp = total_prefix; a.ts = total_suffix;
+  a.h_q = h_q; a.h_kv = h_kv; a.rot = rotary_dim; a.flags = flags;
+  a.log2_base = std::log2(base);
+  for (int t = 0; t < 4; ++t) { a.src[t] = ins[t]; a.dst[t] = outs[t]; }
+  {
+    Timed tp(PG_K_PLAN, st);
+    if ((rc = launch_rope_plan(L, ws, n_groups, n_suffixes, total_prefix, total_suffix, cu_prefix_lens,
+                               cu_suffix_lens, group_sizes, st)))
+      return rc;
+  }
+  const dim3 grid((unsigned)rows), block(pg::kRopeThreads);
+  Timed tm(PG_K_ROPE, st);
+  if (dtype == PG_BF16) {
+    if (head_dim == 128) hipLaunchKernelGGL((pg::rope_kernel<pg::bf16, 128>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((pg::rope_kernel<pg::bf16, 64>), grid, block, 0, st, a);
+  } else {
+    if (head_dim == 128) hipLaunchKernelGGL((pg::rope_kernel<float, 128>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((pg::rope_kernel<float, 64>), grid, block, 0, st, a);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "rope launch");
+  return PG_OK;
+}
+
+int pg_grouped_positions(int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                         const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                         int32_t* pos_pre, int32_t* pos_suf, void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  int rc = check_grouping(n_groups, n_suffixes, total_prefix, total_suffix, cu_prefix_lens, cu_suffix_lens,
+                          group_sizes);
+  if (rc) return rc;
+  if ((total_prefix > 0 && !pos_pre) || (total_suffix > 0 && !pos_suf))
+    return fail(PG_EINVAL, "a position array is NULL");
+  const RopeLayout L = rope_layout(n_groups);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(PG_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
+  if ((rc = device_ready())) return rc;
+  const int rows = total_prefix + total_suffix;
+  if (rows == 0) return PG_OK;
+  hipStream_t st = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  if ((rc = launch_rope_plan(L, ws, n_groups, n_suffixes, total_prefix, total_suffix, cu_prefix_lens,
+                             cu_suffix_lens, group_sizes, st)))
+    return rc;
+  pg::RopeArgs a{};
+  a.cu_p = cu_prefix_lens; a.cu_s = cu_suffix_lens;
+  a.hdr = (const pg::PlanHeader*)(ws + L.hdr);
+  a.ginfo = (const pg::GroupInfoEx*)(ws + L.ginfo);
+  a.ng = n_groups; a.ns = n_suffixes; a.tp = total_prefix; a.ts = total_suffix;
+  a.pos_out[0] = pos_pre; a.pos_out[1] = pos_suf;
+  hipLaunchKernelGGL(pg::positions_kernel, dim3((unsigned)ceil_div_l(rows, 256)), dim3(256), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "positions launch");
   return PG_OK;
 }
 

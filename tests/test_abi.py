@@ -93,3 +93,53 @@ def test_valid_call_without_a_gpu_reports_hip_error():
         pytest.skip("a GPU is present")
     assert _call_fwd() == 4
     assert "hip" in binding.lib().pg_last_error().decode().lower()
+
+
+def _call_rope(**over):
+    args = dict(dtype=0, ng=1, ns=2, tp=8, ts=6, cu=16, h_q=4, h_kv=2, d=128, rot=128, base=10000.0, flags=0,
+                ptr=256, ws=256, ws_bytes=1 << 20)
+    args.update(over)
+    p = lambda v: ctypes.c_void_p(v) if v else None  # noqa: E731
+    L = binding.lib()
+    return L.pg_rope(args["dtype"], args["ng"], args["ns"], args["tp"], args["ts"], p(args["cu"]), p(args["cu"]),
+                     p(args["cu"]), args["h_q"], args["h_kv"], args["d"], args["rot"], args["base"], args["flags"],
+                     *[p(args["ptr"])] * 8, p(args["ws"]), args["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(dtype=3), 2),
+    (dict(d=96, rot=96), 2),
+    (dict(rot=8), 2),
+    (dict(rot=40), 2),
+    (dict(d=64, rot=128), 2),
+    (dict(h_q=0, h_kv=0), 1),
+    (dict(h_q=600, h_kv=0), 2),
+    (dict(base=0.0), 1),
+    (dict(base=float("inf")), 1),
+    (dict(flags=4), 1),
+    (dict(ptr=0), 1),
+    (dict(ptr=264), 1),          # not 16-byte aligned
+    (dict(cu=0), 1),
+    (dict(ng=0), 1),
+    (dict(ws=0), 3),
+    (dict(ws_bytes=8), 3),
+])
+def test_rope_host_validation(over, status):
+    assert _call_rope(**over) == status
+    assert binding.lib().pg_last_error().decode() != ""
+
+
+def test_rope_workspace_and_positions_validation():
+    L = binding.lib()
+    assert L.pg_rope_workspace_size(1) > 0 and L.pg_rope_workspace_size(1000) > L.pg_rope_workspace_size(1)
+    assert L.pg_rope_workspace_size(-1) == 0
+    p = ctypes.c_void_p(256)
+    assert L.pg_grouped_positions(1, 2, 8, 6, p, p, p, None, p, p, 1 << 20, None) == 1   # NULL pos_pre
+    assert L.pg_grouped_positions(1, 2, 8, 6, p, p, p, p, p, p, 8, None) == 3            # workspace too small
+
+
+def test_rope_without_a_gpu_reports_hip_error():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    assert _call_rope() == 4
