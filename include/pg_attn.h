@@ -116,6 +116,31 @@ int pg_attn_bwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int t
                 void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The same two calls on the single-buffer layout of Eq. (2): every tensor is one
+ * buffer whose rows are, group after group, the group's prefix rows followed by
+ * the response rows of its members in member order ([P; R_1; ...; R_G]), so
+ * q, k, v, o, do, dq, dk, dv are [total_prefix + total_suffix, h, head_dim] and
+ * lse is [h_q, total_prefix + total_suffix] fp32 in the same row order. This is
+ * the layout the paper feeds (X_ours); splitting it into prefix and response
+ * parts ("ungroup") and putting the outputs back ("group") cost nothing. The
+ * grouping arrays, sizes, numerics, workspace sizes (same queries), determinism
+ * and error behaviour are those of pg_attn_fwd / pg_attn_bwd; results are
+ * bitwise identical to theirs on the same rows.
+ */
+int pg_attn_fwd_xours(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                      const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                      int h_q, int h_kv, int head_dim, float softmax_scale,
+                      const void* q, const void* k, const void* v, void* o, float* lse,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+int pg_attn_bwd_xours(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                      const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                      int h_q, int h_kv, int head_dim, float softmax_scale,
+                      const void* q, const void* k, const void* v, const void* o, const float* lse,
+                      const void* d_o, void* dq, void* dk, void* dv,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Rotary position embedding with grouped position ids, the step before the
  * attention calls (Algorithm 1 takes q and k already rotary-encoded). Each
  * token gets the position it has in the Repeated-Prefix Forward (Section 2,

@@ -26,6 +26,8 @@ SIGNATURES = {
     "pg_attn_bwd_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
     "pg_attn_fwd": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 10 + [_P, _Z, _P]),
     "pg_attn_bwd": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 18 + [_P, _Z, _P]),
+    "pg_attn_fwd_xours": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 5 + [_P, _Z, _P]),
+    "pg_attn_bwd_xours": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 9 + [_P, _Z, _P]),
     "pg_rope_workspace_size": (_Z, [_I]),
     "pg_rope": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _I, ctypes.c_double, _I] + [_P] * 8 + [_P, _Z, _P]),
     "pg_grouped_positions": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _Z, _P]),
@@ -157,6 +159,48 @@ def bwd(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, o_pre, o_suf, lse_pre, lse_suf
         _ptr(o_pre), _ptr(o_suf), _ptr(lse_pre), _ptr(lse_suf), _ptr(do_pre), _ptr(do_suf),
         *[_ptr(t) for t in out],
         _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(torch, dev))
+    _check(st)
+    return out
+
+
+def fwd_xours(q, k, v, cu_prefix, cu_suffix, group_sizes, total_prefix, scale, out=None, workspace=None):
+    """Forward on the single-buffer layout of Eq. (2) (pg_attn_fwd_xours): q [rows, h_q, d], k, v
+    [rows, h_kv, d], rows grouped as [P; R_1; ...; R_G] per group. Returns (o, lse [h_q, rows])."""
+    import torch
+    ng, ns = group_sizes.numel(), cu_suffix.numel() - 1
+    rows, hq, d = q.shape
+    hkv = k.shape[1]
+    tp, ts = int(total_prefix), rows - int(total_prefix)
+    if out is None:
+        out = (torch.empty_like(q), torch.empty((hq, rows), device=q.device, dtype=torch.float32))
+    if workspace is None:
+        workspace = torch.empty(workspace_bytes("fwd", ng, ns, tp, ts, hq, hkv, d), device=q.device,
+                                dtype=torch.uint8)
+    o, lse = out
+    st = lib().pg_attn_fwd_xours(_dtype_code(torch, q.dtype), ng, ns, tp, ts, _ptr(cu_prefix), _ptr(cu_suffix),
+                                 _ptr(group_sizes), hq, hkv, d, float(scale), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                                 _ptr(lse), _ptr(workspace), workspace.numel(), _stream(torch, q.device))
+    _check(st)
+    return o, lse
+
+
+def bwd_xours(q, k, v, o, lse, d_o, cu_prefix, cu_suffix, group_sizes, total_prefix, scale, out=None,
+              workspace=None):
+    """Backward on the single-buffer layout (pg_attn_bwd_xours). Returns (dq, dk, dv) in that layout."""
+    import torch
+    ng, ns = group_sizes.numel(), cu_suffix.numel() - 1
+    rows, hq, d = q.shape
+    hkv = k.shape[1]
+    tp, ts = int(total_prefix), rows - int(total_prefix)
+    if out is None:
+        out = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v))
+    if workspace is None:
+        workspace = torch.empty(workspace_bytes("bwd", ng, ns, tp, ts, hq, hkv, d), device=q.device,
+                                dtype=torch.uint8)
+    st = lib().pg_attn_bwd_xours(_dtype_code(torch, q.dtype), ng, ns, tp, ts, _ptr(cu_prefix), _ptr(cu_suffix),
+                                 _ptr(group_sizes), hq, hkv, d, float(scale), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                                 _ptr(lse), _ptr(d_o), *[_ptr(t) for t in out], _ptr(workspace),
+                                 workspace.numel(), _stream(torch, q.device))
     _check(st)
     return out
 

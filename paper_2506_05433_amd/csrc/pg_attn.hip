@@ -39,7 +39,7 @@ long ceil_div_l(long a, long b) { return (a + b - 1) / b; }
 
 // Workspace layout shared by the forward and backward calls.
 struct Layout {
-  size_t hdr, ginfo, qoff, kvoff, qtiles, qorder, kvtiles, kvorder, seg, dsum, part, total;
+  size_t hdr, ginfo, qoff, kvoff, qtiles, qorder, kvtiles, kvorder, seg, dsum, part, xrow, total;
   long max_q, max_kv;
   int kv_chunks;
 };
@@ -73,6 +73,7 @@ Layout make_layout(int ng, int ns, int tp, int ts, int h_q, int h_kv, int d, boo
   L.seg = take(sizeof(int) * (size_t)(ts > 0 ? ts : 1));
   L.dsum = bwd ? take(sizeof(float) * (size_t)h_q * (size_t)(tp + ts > 0 ? tp + ts : 1)) : off;
   L.part = (bwd && L.kv_chunks > 1) ? take(sizeof(float) * (size_t)L.kv_chunks * 2 * tp * h_kv * d) : off;
+  L.xrow = bwd ? take(sizeof(int) * (size_t)(tp + ts > 0 ? tp + ts : 1)) : off;
   L.total = off;
   return L;
 }
@@ -164,7 +165,7 @@ bool debug_validate() {
 
 // Runs the planner kernels. `bwd` also builds the key/value tile list.
 int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p, const int32_t* cu_s,
-                const int32_t* gsz, hipStream_t st, bool bwd) {
+                const int32_t* gsz, hipStream_t st, bool bwd, bool xl) {
   Timed tm(PG_K_PLAN, st);
   auto* hdr = (pg::PlanHeader*)(ws + L.hdr);
   auto* gi = (pg::GroupInfoEx*)(ws + L.ginfo);
@@ -192,6 +193,10 @@ int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p,
   if (c.ts > 0) {
     hipLaunchKernelGGL(pg::seg_start_kernel, dim3((unsigned)ceil_div_l(c.ts, 256)), dim3(256), 0, st, cu_s, c.ns,
                        c.ts, hdr, (int*)(ws + L.seg));
+  }
+  if (bwd && xl && c.tp + c.ts > 0) {
+    hipLaunchKernelGGL(pg::xrow_kernel, dim3((unsigned)ceil_div_l((long)c.tp + c.ts, 256)), dim3(256), 0, st, cu_p,
+                       cu_s, c.ng, c.ns, c.tp, c.ts, hdr, gi, (int*)(ws + L.xrow));
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "planner launch");
@@ -236,6 +241,88 @@ void launch_bwd(const pg::BwdArgs& a, long max_q, long max_kv, hipStream_t st) {
   }
 }
 
+
+
+// The calls' bodies after argument checks; xl selects the single-buffer layout of Eq. (2)
+// (the caller then passes the same buffer for the prefix and response sides).
+int fwd_impl(const Common& c, const int32_t* cu_p, const int32_t* cu_s, const int32_t* gsz, const void* q_pre,
+             const void* k_pre, const void* v_pre, const void* q_suf, const void* k_suf, const void* v_suf,
+             void* o_pre, void* o_suf, float* lse_pre, float* lse_suf, bool xl, void* workspace,
+             size_t workspace_bytes, void* stream) {
+  const Layout L = make_layout(c.ng, c.ns, c.tp, c.ts, c.h_q, c.h_kv, c.d, false);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(PG_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
+  int rc = device_ready();
+  if (rc) return rc;
+  if (c.ng == 0) return PG_OK;
+  hipStream_t st = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  if ((rc = launch_plan(c, L, ws, cu_p, cu_s, gsz, st, false, xl))) return rc;
+  pg::FwdArgs a{};
+  a.q_pre = q_pre; a.k_pre = k_pre; a.v_pre = v_pre; a.q_suf = q_suf; a.k_suf = k_suf; a.v_suf = v_suf;
+  a.o_pre = o_pre; a.o_suf = o_suf; a.lse_pre = lse_pre; a.lse_suf = lse_suf;
+  a.hdr = (const pg::PlanHeader*)(ws + L.hdr);
+  a.ginfo = (const pg::GroupInfoEx*)(ws + L.ginfo);
+  a.qtiles = (const pg::TileDesc*)(ws + L.qtiles);
+  a.qorder = (const int*)(ws + L.qorder);
+  a.seg_start = (const int*)(ws + L.seg);
+  a.h_q = c.h_q; a.h_kv = c.h_kv; a.total_prefix = c.tp; a.total_suffix = c.ts;
+  a.scale_log2 = c.scale * pg::kLog2e;
+  a.xl = xl ? 1 : 0;
+  if (c.dtype == PG_BF16) {
+    if (c.d == 128) launch_fwd<pg::bf16, 128>(a, L.max_q, st); else launch_fwd<pg::bf16, 64>(a, L.max_q, st);
+  } else {
+    if (c.d == 128) launch_fwd<float, 128>(a, L.max_q, st); else launch_fwd<float, 64>(a, L.max_q, st);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "forward launch");
+  return PG_OK;
+}
+
+// in: q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, o_pre, o_suf, lse_pre, lse_suf, do_pre, do_suf;
+// out: dq_pre, dk_pre, dv_pre, dq_suf, dk_suf, dv_suf.
+int bwd_impl(const Common& c, const int32_t* cu_p, const int32_t* cu_s, const int32_t* gsz, const void* const* in,
+             void* const* out, bool xl, void* workspace, size_t workspace_bytes, void* stream) {
+  const Layout L = make_layout(c.ng, c.ns, c.tp, c.ts, c.h_q, c.h_kv, c.d, true);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(PG_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
+  int rc = device_ready();
+  if (rc) return rc;
+  if (c.ng == 0) return PG_OK;
+  hipStream_t st = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  if ((rc = launch_plan(c, L, ws, cu_p, cu_s, gsz, st, true, xl))) return rc;
+  pg::BwdArgs a{};
+  a.q_pre = in[0]; a.k_pre = in[1]; a.v_pre = in[2]; a.q_suf = in[3]; a.k_suf = in[4]; a.v_suf = in[5];
+  a.o_pre = in[6]; a.o_suf = in[7]; a.lse_pre = (const float*)in[8]; a.lse_suf = (const float*)in[9];
+  a.do_pre = in[10]; a.do_suf = in[11];
+  a.dq_pre = out[0]; a.dk_pre = out[1]; a.dv_pre = out[2]; a.dq_suf = out[3]; a.dk_suf = out[4]; a.dv_suf = out[5];
+  a.dsum = (float*)(ws + L.dsum);
+  a.part = (float*)(ws + L.part);
+  a.kv_chunks = L.kv_chunks;
+  a.hdr = (const pg::PlanHeader*)(ws + L.hdr);
+  a.ginfo = (const pg::GroupInfoEx*)(ws + L.ginfo);
+  a.qtiles = (const pg::TileDesc*)(ws + L.qtiles);
+  a.qorder = (const int*)(ws + L.qorder);
+  a.kvtiles = (const pg::TileDesc*)(ws + L.kvtiles);
+  a.kvorder = (const int*)(ws + L.kvorder);
+  a.seg_start = (const int*)(ws + L.seg);
+  a.h_q = c.h_q; a.h_kv = c.h_kv; a.total_prefix = c.tp; a.total_suffix = c.ts;
+  a.scale = c.scale;
+  a.scale_log2 = c.scale * pg::kLog2e;
+  a.xl = xl ? 1 : 0;
+  a.xrow = (const int*)(ws + L.xrow);
+  if (c.dtype == PG_BF16) {
+    if (c.d == 128) launch_bwd<pg::bf16, 128>(a, L.max_q, L.max_kv, st);
+    else launch_bwd<pg::bf16, 64>(a, L.max_q, L.max_kv, st);
+  } else {
+    if (c.d == 128) launch_bwd<float, 128>(a, L.max_q, L.max_kv, st);
+    else launch_bwd<float, 64>(a, L.max_q, L.max_kv, st);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "backward launch");
+  return PG_OK;
+}
 
 // ---------------------------------------------------------------- rotary embedding
 // Workspace of the rope / positions calls: the planner's header and per-group ranges.
@@ -336,32 +423,23 @@ int pg_attn_fwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int t
     return fail(PG_EINVAL, "a prefix tensor pointer is NULL");
   if (total_suffix > 0 && (!q_suf || !k_suf || !v_suf || !o_suf || !lse_suf))
     return fail(PG_EINVAL, "a suffix tensor pointer is NULL");
-  const Layout L = make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, false);
-  if (!workspace || workspace_bytes < L.total)
-    return fail(PG_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
-  if ((rc = device_ready())) return rc;
-  if (n_groups == 0) return PG_OK;
-  hipStream_t st = (hipStream_t)stream;
-  char* ws = (char*)workspace;
-  if ((rc = launch_plan(c, L, ws, cu_prefix_lens, cu_suffix_lens, group_sizes, st, false))) return rc;
-  pg::FwdArgs a{};
-  a.q_pre = q_pre; a.k_pre = k_pre; a.v_pre = v_pre; a.q_suf = q_suf; a.k_suf = k_suf; a.v_suf = v_suf;
-  a.o_pre = o_pre; a.o_suf = o_suf; a.lse_pre = lse_pre; a.lse_suf = lse_suf;
-  a.hdr = (const pg::PlanHeader*)(ws + L.hdr);
-  a.ginfo = (const pg::GroupInfoEx*)(ws + L.ginfo);
-  a.qtiles = (const pg::TileDesc*)(ws + L.qtiles);
-  a.qorder = (const int*)(ws + L.qorder);
-  a.seg_start = (const int*)(ws + L.seg);
-  a.h_q = h_q; a.h_kv = h_kv; a.total_prefix = total_prefix; a.total_suffix = total_suffix;
-  a.scale_log2 = softmax_scale * pg::kLog2e;
-  if (dtype == PG_BF16) {
-    if (head_dim == 128) launch_fwd<pg::bf16, 128>(a, L.max_q, st); else launch_fwd<pg::bf16, 64>(a, L.max_q, st);
-  } else {
-    if (head_dim == 128) launch_fwd<float, 128>(a, L.max_q, st); else launch_fwd<float, 64>(a, L.max_q, st);
-  }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return hip_fail(e, "forward launch");
-  return PG_OK;
+  return fwd_impl(c, cu_prefix_lens, cu_suffix_lens, group_sizes, q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, o_pre,
+                  o_suf, lse_pre, lse_suf, false, workspace, workspace_bytes, stream);
+}
+
+int pg_attn_fwd_xours(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                      const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                      int h_q, int h_kv, int head_dim, float softmax_scale,
+                      const void* q, const void* k, const void* v, void* o, float* lse,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  const Common c{dtype, n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, softmax_scale};
+  int rc = check_common(c, cu_prefix_lens, cu_suffix_lens, group_sizes);
+  if (rc) return rc;
+  if (total_prefix + total_suffix > 0 && (!q || !k || !v || !o || !lse))
+    return fail(PG_EINVAL, "a tensor pointer is NULL");
+  return fwd_impl(c, cu_prefix_lens, cu_suffix_lens, group_sizes, q, k, v, q, k, v, o, o, lse, lse, true, workspace,
+                  workspace_bytes, stream);
 }
 
 int pg_attn_bwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
@@ -384,42 +462,26 @@ int pg_attn_bwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int t
   if (total_suffix > 0 && (!q_suf || !k_suf || !v_suf || !o_suf || !lse_suf || !do_suf || !dq_suf || !dk_suf ||
                            !dv_suf))
     return fail(PG_EINVAL, "a suffix tensor pointer is NULL");
-  const Layout L = make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, true);
-  if (!workspace || workspace_bytes < L.total)
-    return fail(PG_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
-  if ((rc = device_ready())) return rc;
-  if (n_groups == 0) return PG_OK;
-  hipStream_t st = (hipStream_t)stream;
-  char* ws = (char*)workspace;
-  if ((rc = launch_plan(c, L, ws, cu_prefix_lens, cu_suffix_lens, group_sizes, st, true))) return rc;
-  pg::BwdArgs a{};
-  a.q_pre = q_pre; a.k_pre = k_pre; a.v_pre = v_pre; a.q_suf = q_suf; a.k_suf = k_suf; a.v_suf = v_suf;
-  a.o_pre = o_pre; a.o_suf = o_suf; a.do_pre = do_pre; a.do_suf = do_suf;
-  a.lse_pre = lse_pre; a.lse_suf = lse_suf;
-  a.dq_pre = dq_pre; a.dk_pre = dk_pre; a.dv_pre = dv_pre; a.dq_suf = dq_suf; a.dk_suf = dk_suf; a.dv_suf = dv_suf;
-  a.dsum = (float*)(ws + L.dsum);
-  a.part = (float*)(ws + L.part);
-  a.kv_chunks = L.kv_chunks;
-  a.hdr = (const pg::PlanHeader*)(ws + L.hdr);
-  a.ginfo = (const pg::GroupInfoEx*)(ws + L.ginfo);
-  a.qtiles = (const pg::TileDesc*)(ws + L.qtiles);
-  a.qorder = (const int*)(ws + L.qorder);
-  a.kvtiles = (const pg::TileDesc*)(ws + L.kvtiles);
-  a.kvorder = (const int*)(ws + L.kvorder);
-  a.seg_start = (const int*)(ws + L.seg);
-  a.h_q = h_q; a.h_kv = h_kv; a.total_prefix = total_prefix; a.total_suffix = total_suffix;
-  a.scale = softmax_scale;
-  a.scale_log2 = softmax_scale * pg::kLog2e;
-  if (dtype == PG_BF16) {
-    if (head_dim == 128) launch_bwd<pg::bf16, 128>(a, L.max_q, L.max_kv, st);
-    else launch_bwd<pg::bf16, 64>(a, L.max_q, L.max_kv, st);
-  } else {
-    if (head_dim == 128) launch_bwd<float, 128>(a, L.max_q, L.max_kv, st);
-    else launch_bwd<float, 64>(a, L.max_q, L.max_kv, st);
-  }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return hip_fail(e, "backward launch");
-  return PG_OK;
+  const void* in[12] = {q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, o_pre, o_suf, lse_pre, lse_suf, do_pre, do_suf};
+  void* out[6] = {dq_pre, dk_pre, dv_pre, dq_suf, dk_suf, dv_suf};
+  return bwd_impl(c, cu_prefix_lens, cu_suffix_lens, group_sizes, in, out, false, workspace, workspace_bytes, stream);
+}
+
+int pg_attn_bwd_xours(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                      const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                      int h_q, int h_kv, int head_dim, float softmax_scale,
+                      const void* q, const void* k, const void* v, const void* o, const float* lse,
+                      const void* d_o, void* dq, void* dk, void* dv,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  const Common c{dtype, n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, softmax_scale};
+  int rc = check_common(c, cu_prefix_lens, cu_suffix_lens, group_sizes);
+  if (rc) return rc;
+  if (total_prefix + total_suffix > 0 && (!q || !k || !v || !o || !lse || !d_o || !dq || !dk || !dv))
+    return fail(PG_EINVAL, "a tensor pointer is NULL");
+  const void* in[12] = {q, k, v, q, k, v, o, o, lse, lse, d_o, d_o};
+  void* out[6] = {dq, dk, dv, dq, dk, dv};
+  return bwd_impl(c, cu_prefix_lens, cu_suffix_lens, group_sizes, in, out, true, workspace, workspace_bytes, stream);
 }
 
 int pg_timing_start(void) {

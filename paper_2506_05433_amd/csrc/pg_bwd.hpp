@@ -36,6 +36,10 @@ struct BwdArgs {
   const int* seg_start;
   int h_q, h_kv, total_prefix, total_suffix;
   float scale, scale_log2;
+  // 1: single-buffer layout of Eq. (2) (see FwdArgs::xl); xrow maps packed rows (prefix
+  // rows, then response rows) to tensor rows for the kernels that sweep rows
+  int xl;
+  const int* xrow;
 };
 
 // ------------------------------------------------------------------ Dsum = rowsum(dO * O)
@@ -49,7 +53,7 @@ __global__ void __launch_bounds__(256) bwd_dot_kernel(const BwdArgs a) {
   if (item >= (long)rows * a.h_q) return;
   const int row = (int)(item / a.h_q), head = (int)(item % a.h_q);
   const bool pre = row < a.total_prefix;
-  const int r = pre ? row : row - a.total_prefix;
+  const int r = a.xl ? a.xrow[row] : (pre ? row : row - a.total_prefix);
   const T* O = (const T*)(pre ? a.o_pre : a.o_suf) + ((size_t)r * a.h_q + head) * D + sub * EPL;
   const T* G = (const T*)(pre ? a.do_pre : a.do_suf) + ((size_t)r * a.h_q + head) * D + sub * EPL;
   float acc = 0.f;
@@ -107,6 +111,11 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
   const TileDesc td = a.kvtiles[a.kvorder[rank]];
   const GroupInfoEx gi = a.ginfo[td.group];
   const bool kv_suffix = td.kind == 1;
+  // tensor row offsets of this group's prefix and response rows (single-buffer layout)
+  const int xo_pre = a.xl ? gi.s0 : 0, xo_suf = a.xl ? gi.p1 : 0;
+  const int xk = kv_suffix ? xo_suf : xo_pre;
+  const int lse_ld_pre = a.xl ? a.total_prefix + a.total_suffix : a.total_prefix;
+  const int lse_ld_suf = a.xl ? a.total_prefix + a.total_suffix : a.total_suffix;
   const int ratio = a.h_q / a.h_kv;
   const int rows_all = a.total_prefix + a.total_suffix;
 
@@ -125,7 +134,7 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
   Frag kv[KK];
   {
     const T* B = (const T*)(pwave ? (kv_suffix ? a.k_suf : a.k_pre) : (kv_suffix ? a.v_suf : a.v_pre));
-    const size_t off = ((size_t)key_c * a.h_kv + kvh) * D + 8 * hh;
+    const size_t off = ((size_t)(key_c + xk) * a.h_kv + kvh) * D + 8 * hh;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) kv[kk] = E::global_row(B + off + 16 * kk, kvalid);
   }
@@ -192,15 +201,15 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
   auto issue = [&](const TileInfo& ti, int it) {  // `it` selects the buffer
     const T* Qs = (const T*)(ti.qsuf ? a.q_suf : a.q_pre);
     const T* Gs = (const T*)(ti.qsuf ? a.do_suf : a.do_pre);
-    const size_t off = ((size_t)ti.q0 * a.h_q + ti.hq) * D;
+    const size_t off = ((size_t)(ti.q0 + (ti.qsuf ? xo_suf : xo_pre)) * a.h_q + ti.hq) * D;
     ldq.load(smem[it % NBUF][0], Qs + off, a.h_q * D, ti.qend - ti.q0);
     ldo.load(smem[it % NBUF][1], Gs + off, a.h_q * D, ti.qend - ti.q0);
     if (tid < BQ) {
       const int q = ti.q0 + tid;
       const bool v = q < ti.qend;
       const float* L = ti.qsuf ? a.lse_suf : a.lse_pre;
-      const int tot = ti.qsuf ? a.total_suffix : a.total_prefix;
-      pf_lse = v ? L[(size_t)ti.hq * tot + q] * kLog2e : INFINITY;
+      const int ld = ti.qsuf ? lse_ld_suf : lse_ld_pre;
+      pf_lse = v ? L[(size_t)ti.hq * ld + q + (ti.qsuf ? xo_suf : xo_pre)] * kLog2e : INFINITY;
       pf_dsum = v ? a.dsum[(size_t)ti.hq * rows_all + (ti.qsuf ? a.total_prefix : 0) + q] : 0.f;
       pf_seg = (v && ti.qsuf) ? a.seg_start[q] : 0;
     }
@@ -349,7 +358,7 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     return;
   }
   T* out = (T*)(pwave ? (kv_suffix ? a.dv_suf : a.dv_pre) : (kv_suffix ? a.dk_suf : a.dk_pre)) +
-           ((size_t)key * a.h_kv + kvh) * D;
+           ((size_t)(key + xk) * a.h_kv + kvh) * D;
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -372,7 +381,13 @@ __global__ void __launch_bounds__(256) kv_reduce_kernel(const BwdArgs a) {
   const float* src = a.part + (size_t)which * a.total_prefix * a.h_kv * D + 4 * e;
   f32x4 s = *(const f32x4*)src;
   for (int c = 1; c < a.kv_chunks; ++c) s += *(const f32x4*)(src + c * stride);
-  T* dst = (T*)(which ? a.dv_pre : a.dk_pre) + 4 * e;
+  long de = e;  // destination float4 index: the packed prefix row mapped to its tensor row
+  if (a.xl) {
+    const long per_row = (long)a.h_kv * D / 4;
+    const long t = e / per_row;
+    de = (long)a.xrow[t] * per_row + (e - t * per_row);
+  }
+  T* dst = (T*)(which ? a.dv_pre : a.dk_pre) + 4 * de;
   Elt<T>::store4(dst, s[0], s[1], s[2], s[3]);
 }
 
@@ -401,6 +416,9 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
   const int kvh = head / (a.h_q / a.h_kv);
   const bool suffix = td.kind == 1;
   const int rows_all = a.total_prefix + a.total_suffix;
+  // tensor row offsets of this group's prefix and response rows (single-buffer layout)
+  const int xo_pre = a.xl ? gi.s0 : 0, xo_suf = a.xl ? gi.p1 : 0;
+  const int xq = suffix ? xo_suf : xo_pre;
 
   const int tid = threadIdx.x, wave = uniform(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hh = lane >> 5;
@@ -415,7 +433,7 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
   const T* G = (const T*)(suffix ? a.do_suf : a.do_pre);
   Frag qf[KK], gf[KK];
   {
-    const size_t off = ((size_t)qrow_c * a.h_q + head) * D + 8 * hh;
+    const size_t off = ((size_t)(qrow_c + xq) * a.h_q + head) * D + 8 * hh;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       qf[kk] = E::global_row(Q + off + 16 * kk, qvalid);
@@ -423,8 +441,8 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
     }
   }
   const float* L = suffix ? a.lse_suf : a.lse_pre;
-  const int tot = suffix ? a.total_suffix : a.total_prefix;
-  const float lse2 = L[(size_t)head * tot + qrow_c] * kLog2e;
+  const int ld = a.xl ? rows_all : (suffix ? a.total_suffix : a.total_prefix);
+  const float lse2 = L[(size_t)head * ld + qrow_c + xq] * kLog2e;
   const float dsum = a.dsum[(size_t)head * rows_all + (suffix ? a.total_prefix : 0) + qrow_c];
   const int seg_q = suffix ? a.seg_start[qrow_c] : 0;
   const int seg_w_lo = (suffix && wave_active) ? a.seg_start[wq0] : 0;
@@ -448,8 +466,9 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
-    ldk.load(smem[j & 1][0], (segA ? Kp : Ks) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0);
-    ldv.load(smem[j & 1][1], (segA ? Vp : Vs) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0);
+    const size_t kx = (size_t)(k0 + (segA ? xo_pre : xo_suf));
+    ldk.load(smem[j & 1][0], (segA ? Kp : Ks) + kx * kvstride + kvh * D, kvstride, kend - k0);
+    ldv.load(smem[j & 1][1], (segA ? Vp : Vs) + kx * kvstride + kvh * D, kvstride, kend - k0);
   };
 
   f32x16 acc[DB];
@@ -531,7 +550,7 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
   }
 
   if (!wave_active || !qvalid) return;
-  T* dQ = (T*)(suffix ? a.dq_suf : a.dq_pre) + ((size_t)qrow * a.h_q + head) * D;
+  T* dQ = (T*)(suffix ? a.dq_suf : a.dq_pre) + ((size_t)(qrow + xq) * a.h_q + head) * D;
   const float sc = a.scale;
 #pragma unroll
   for (int db = 0; db < DB; ++db)

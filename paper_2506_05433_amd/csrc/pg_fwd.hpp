@@ -30,6 +30,10 @@ struct FwdArgs {
   const int* seg_start;
   int h_q, h_kv, total_prefix, total_suffix;
   float scale_log2;  // softmax_scale * log2(e)
+  // 1: every tensor is one buffer in the layout of Eq. (2) (per group [P; R_1; ...; R_G],
+  // groups one after another; *_pre and *_suf point at the same buffer, lse is
+  // [h_q, total_prefix + total_suffix]); 0: separate prefix and response buffers.
+  int xl;
 };
 
 constexpr int kFwdBM = 128;  // query rows per workgroup
@@ -56,6 +60,9 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
   const GroupInfoEx gi = a.ginfo[td.group];
   const int kvh = head / (a.h_q / a.h_kv);
   const bool suffix = td.kind == 1;
+  // tensor row offsets of this group's prefix and response rows (single-buffer layout)
+  const int xo_pre = a.xl ? gi.s0 : 0, xo_suf = a.xl ? gi.p1 : 0;
+  const int xq = suffix ? xo_suf : xo_pre;
 
   const int tid = threadIdx.x, wave = uniform(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hh = lane >> 5;
@@ -69,7 +76,7 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
   const T* Q = (const T*)(suffix ? a.q_suf : a.q_pre);
   Frag qf[KK];
   {
-    const T* qp = Q + ((size_t)qrow_c * a.h_q + head) * D + 8 * hh;
+    const T* qp = Q + ((size_t)(qrow_c + xq) * a.h_q + head) * D + 8 * hh;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) qf[kk] = E::global_row(qp + 16 * kk, qvalid);
   }
@@ -97,8 +104,9 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
-    const T* kb = (segA ? Kp : Ks) + (size_t)k0 * kvstride + kvh * D;
-    const T* vb = (segA ? Vp : Vs) + (size_t)k0 * kvstride + kvh * D;
+    const size_t kx = (size_t)(k0 + (segA ? xo_pre : xo_suf));
+    const T* kb = (segA ? Kp : Ks) + kx * kvstride + kvh * D;
+    const T* vb = (segA ? Vp : Vs) + kx * kvstride + kvh * D;
     ldk.load(smem[j & 1][0], kb, kvstride, kend - k0);
     ldv.load(smem[j & 1][1], vb, kvstride, kend - k0);
   };
@@ -218,7 +226,7 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
   const float inv = 1.f / l_tot;
   if (qvalid) {
     T* O = (T*)(suffix ? a.o_suf : a.o_pre);
-    T* op = O + ((size_t)qrow * a.h_q + head) * D;
+    T* op = O + ((size_t)(qrow + xq) * a.h_q + head) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -230,8 +238,8 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
     if (hh == 0) {
       const float lse = (m_run + fast_log2(l_tot)) * kLn2;
       float* L = suffix ? a.lse_suf : a.lse_pre;
-      const int tot = suffix ? a.total_suffix : a.total_prefix;
-      L[(size_t)head * tot + qrow] = lse;
+      const int ld = a.xl ? a.total_prefix + a.total_suffix : (suffix ? a.total_suffix : a.total_prefix);
+      L[(size_t)head * ld + qrow + xq] = lse;
     }
   }
 }

@@ -209,4 +209,27 @@ __global__ void seg_start_kernel(const int* __restrict__ cu_s, int ns, int ts, c
   seg_start[r] = cu_s[m];
 }
 
+// Row map of the single-buffer layout of Eq. (2) (per group [P; R_1; ...; R_G], groups
+// one after another): xrow[t] for packed prefix row t, xrow[total_prefix + s] for packed
+// response row s. Prefix row t of group g is preceded by the responses of the earlier
+// groups (s0 of g rows); response row s of group g by the prefixes of groups 0..g (p1).
+__global__ void xrow_kernel(const int* __restrict__ cu_p, const int* __restrict__ cu_s, int ng, int ns, int tp,
+                            int ts, const PlanHeader* hdr, const GroupInfoEx* __restrict__ ginfo, int* xrow) {
+  const int row = blockIdx.x * blockDim.x + threadIdx.x;
+  if (row >= tp + ts || hdr->error) return;
+  if (row < tp) {
+    const int g = upper_index(cu_p, 0, ng, row);
+    xrow[row] = row + ginfo[g].s0;
+    return;
+  }
+  const int s = row - tp;
+  const int m = upper_index(cu_s, 0, ns, s);
+  int lo = 0, hi = ng;  // the group of member m: the last group whose members start at or before m
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (ginfo[mid].m0 <= m) lo = mid; else hi = mid;
+  }
+  xrow[row] = s + ginfo[lo].p1;
+}
+
 }  // namespace pg

@@ -143,3 +143,11 @@ def test_rope_without_a_gpu_reports_hip_error():
     if torch.cuda.is_available():
         pytest.skip("a GPU is present")
     assert _call_rope() == 4
+
+
+def test_xours_validation():
+    L = binding.lib()
+    p = ctypes.c_void_p(256)
+    # a NULL tensor is rejected before launch; a short workspace too
+    assert L.pg_attn_fwd_xours(0, 1, 2, 8, 6, p, p, p, 4, 2, 128, 0.125, p, p, None, p, p, p, 1 << 30, None) == 1
+    assert L.pg_attn_bwd_xours(0, 1, 2, 8, 6, p, p, p, 4, 2, 128, 0.125, *[p] * 9, p, 16, None) == 3

@@ -1,0 +1,84 @@
+"""GPU checks of the single-buffer layout of Eq. (2) (pg_attn_fwd_xours / pg_attn_bwd_xours).
+
+Every tensor is one buffer holding, group after group, the group's prefix rows and then its members'
+response rows. The calls run the same kernels, plan and arithmetic as the split-layout calls, so on the same
+rows their results must be bitwise identical; one case is also compared with the oracle directly.
+"""
+import numpy as np
+import pytest
+
+from oracle import grouped_oracle
+from paper_2506_05433_amd.inputs import make_problem
+from tests._parity import check, host_view, to_host
+from tests.test_gpu_parity import SMALL
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _dev():
+    from paper_2506_05433_amd import binding
+    assert torch.cuda.is_available(), "GPU test needs a GPU"
+    binding.lib()
+    return binding
+
+
+def xours_order(prob):
+    """Packed row (prefix rows 0..tp-1, then response rows tp..) of every row of the single buffer."""
+    cu_p, cu_s = prob.cu_prefix, prob.cu_suffix
+    tp = prob.total_prefix
+    order, m = [], 0
+    for g, gs in enumerate(prob.group_sizes):
+        order.append(np.arange(cu_p[g], cu_p[g + 1]))
+        order.append(tp + np.arange(cu_s[m], cu_s[m + int(gs)]))
+        m += int(gs)
+    return np.concatenate(order).astype(np.int64) if order else np.zeros(0, np.int64)
+
+
+def _run_both(prob):
+    binding = _dev()
+    print(f"[xours] {prob.dtype} P={list(prob.prefix_lens)[:6]} G={list(prob.group_sizes)[:6]} "
+          f"h={prob.h_q}/{prob.h_kv} d={prob.head_dim}", flush=True)
+    dev = binding.to_device(prob, "cuda")
+    f = binding.run_fwd(dev)
+    g = binding.run_bwd(dev, f)
+    order = torch.as_tensor(xours_order(prob), device="cuda")
+    x = {n: torch.cat([dev[n + "_pre"], dev[n + "_suf"]])[order] for n in ("q", "k", "v", "do")}
+    grp = (dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], prob.total_prefix, dev["scale"])
+    o, lse = binding.fwd_xours(x["q"], x["k"], x["v"], *grp)
+    dq, dk, dv = binding.bwd_xours(x["q"], x["k"], x["v"], o, lse, x["do"], *grp)
+    torch.cuda.synchronize()
+    split = {"o": torch.cat([f[0], f[1]]), "lse": torch.cat([f[2], f[3]], dim=1), "dq": torch.cat([g[0], g[3]]),
+             "dk": torch.cat([g[1], g[4]]), "dv": torch.cat([g[2], g[5]])}
+    got = {"o": o, "lse": lse, "dq": dq, "dk": dk, "dv": dv}
+    for n in got:
+        ref = split[n][:, order] if n == "lse" else split[n][order]
+        assert torch.equal(got[n], ref), f"{n}: single-buffer result differs from the split layout"
+    return got, order
+
+
+@pytest.mark.parametrize("case", range(len(SMALL)))
+def test_xours_bitwise_equals_split(case):
+    lengths, hq, hkv, d, dt = SMALL[case]
+    prob = make_problem("single_group", seed=300 + case, lengths=lengths, h_q=hq, h_kv=hkv, head_dim=d, dtype=dt,
+                        scale=1.0 / np.sqrt(d))
+    _run_both(prob)
+
+
+def test_xours_single_group_workload():
+    _run_both(make_problem("single_group", seed=0))
+
+
+def test_xours_against_oracle():
+    prob = make_problem("single_group", seed=301, lengths=((257, 0, 40), (3, 2, 0), (129, 128, 1, 300, 0)),
+                        h_q=4, h_kv=2, head_dim=64, dtype="fp32", scale=0.125)
+    got, order = _run_both(prob)
+    ref = grouped_oracle(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, host_view(prob), prob.scale,
+                         grads=True)
+    o = order.cpu().numpy()
+    for n in ("o", "dq", "dk", "dv"):
+        packed = np.concatenate([ref[n + "_pre"], ref[n + "_suf"]])
+        check(n + "_xours", to_host(got[n]), packed[o], "fp32")
+    lse = np.concatenate([ref["lse_pre"], ref["lse_suf"]], axis=1)
+    check("lse_xours", to_host(got["lse"]), lse[:, o], "fp32")
