@@ -93,6 +93,40 @@ def alloc(binding, torch, dev, prob):
     return bufs
 
 
+def time_last(binding, torch, dev, prob, steps, warmup):
+    """The final-token forward (every member's last query only) on this workload.
+
+    HBM-bound: the algorithmic traffic is every key and value row read once, the members' final query rows
+    read once, and their outputs (and fp32 log-sum-exp) written once; the matrix work is a few GFLOP.
+    """
+    ns = len(prob.suffix_lens)
+    el = 2 if prob.dtype == "bf16" else 4
+    names = ("q_pre", "k_pre", "v_pre", "q_suf", "k_suf", "v_suf")
+    outs = (torch.empty((ns, prob.h_q, prob.head_dim), device="cuda", dtype=dev["q_pre"].dtype),
+            torch.empty((prob.h_q, ns), device="cuda", dtype=torch.float32))
+    nbytes_ws = int(binding.lib().pg_attn_fwd_last_workspace_size(len(prob.prefix_lens), ns, prob.total_prefix,
+                                                                  prob.total_suffix, prob.h_q, prob.h_kv,
+                                                                  prob.head_dim))
+    ws = torch.empty(nbytes_ws, device="cuda", dtype=torch.uint8)
+    call = lambda: binding.fwd_last(*[dev[n] for n in names], dev["cu_prefix"], dev["cu_suffix"],  # noqa: E731
+                                    dev["group_sizes"], dev["scale"], out=outs, workspace=ws)
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    binding.timing_start()
+    for _ in range(steps):
+        call()
+    torch.cuda.synchronize()
+    binding.timing_stop()
+    n, tot = binding.timing_get("last")
+    ms = tot / n
+    rows = prob.total_prefix + prob.total_suffix
+    nbytes = 2 * rows * prob.h_kv * prob.head_dim * el + 2 * ns * prob.h_q * prob.head_dim * el + ns * prob.h_q * 4
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"kernel": "last (+ merge)", "ms": round(ms, 4), "bytes": nbytes, "achieved_GBps": round(gbs, 1),
+            "peak_GBps": 8000.0, "frac": round(gbs / 8000.0, 4), "bound": "hbm", "queries": ns * prob.h_q}
+
+
 def time_rope(binding, torch, dev, prob, steps, warmup):
     """The grouped-position rotary embedding of q and k (both sides) on this workload, out of place.
 
@@ -253,6 +287,7 @@ def main():
                      "traffic": recorded_traffic(dom, wl.name), "source_sha": kernel_source_sha()},
     }
     out["rope"] = time_rope(binding, torch, dev, prob, args.steps, args.warmup)
+    out["last"] = time_last(binding, torch, dev, prob, args.steps, args.warmup)
     if not args.no_repeated:
         rep = repeated_layout(prob)
         del dev, bufs

@@ -141,6 +141,30 @@ int pg_attn_bwd_xours(int dtype, int n_groups, int n_suffixes, int total_prefix,
                       void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Forward of the final token of every member only (Section 2, "Further
+ * discussion": multi-QA judging, where a long response is the shared prefix,
+ * each short question a member, and predictions come from the hidden state at
+ * each question's final token). For member i the query is the last row of the
+ * sequence [P; R_i] (its last response row, or the group's last prefix row when
+ * the response is empty); it attends to the whole prefix and to all of R_i, as
+ * in pg_attn_fwd. Outputs: o_last [n_suffixes, h_q, head_dim] (dtype of the
+ * inputs) and lse_last [h_q, n_suffixes] fp32 (natural log). A member whose
+ * sequence is empty (no prefix, no response) gets zeros and lse = -inf.
+ * Inputs, grouping arrays, sizes and errors as for pg_attn_fwd; additionally
+ * h_q / h_kv <= 128. Workspace: pg_attn_fwd_last_workspace_size(...) bytes
+ * (it holds per-chunk fp32 partial results). Deterministic.
+ */
+size_t pg_attn_fwd_last_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q,
+                                       int h_kv, int head_dim);
+
+int pg_attn_fwd_last(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                     const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                     int h_q, int h_kv, int head_dim, float softmax_scale,
+                     const void* q_pre, const void* k_pre, const void* v_pre,
+                     const void* q_suf, const void* k_suf, const void* v_suf,
+                     void* o_last, float* lse_last, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Rotary position embedding with grouped position ids, the step before the
  * attention calls (Algorithm 1 takes q and k already rotary-encoded). Each
  * token gets the position it has in the Repeated-Prefix Forward (Section 2,
@@ -203,7 +227,8 @@ typedef enum {
   PG_K_BWD_DOT = 2,  /* backward: rowsum(dO * O)                              */
   PG_K_DKDV = 3,     /* backward: dK, dV (key-stationary, G-way prefix sum)   */
   PG_K_DQ = 4,       /* backward: dQ (query-stationary)                       */
-  PG_K_ROPE = 5      /* rotary embedding kernel of pg_rope                    */
+  PG_K_ROPE = 5,     /* rotary embedding kernel of pg_rope                    */
+  PG_K_LAST = 6      /* pg_attn_fwd_last: chunk kernel and merge, one interval */
 } pg_kernel;
 
 int pg_timing_start(void);

@@ -28,6 +28,8 @@ SIGNATURES = {
     "pg_attn_bwd": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 18 + [_P, _Z, _P]),
     "pg_attn_fwd_xours": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 5 + [_P, _Z, _P]),
     "pg_attn_bwd_xours": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 9 + [_P, _Z, _P]),
+    "pg_attn_fwd_last_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
+    "pg_attn_fwd_last": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 8 + [_P, _Z, _P]),
     "pg_rope_workspace_size": (_Z, [_I]),
     "pg_rope": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _I, ctypes.c_double, _I] + [_P] * 8 + [_P, _Z, _P]),
     "pg_grouped_positions": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _Z, _P]),
@@ -60,7 +62,7 @@ def lib():
     return _lib
 
 
-KERNELS = {"plan": 0, "fwd": 1, "bwd_dot": 2, "dkdv": 3, "dq": 4, "rope": 5}
+KERNELS = {"plan": 0, "fwd": 1, "bwd_dot": 2, "dkdv": 3, "dq": 4, "rope": 5, "last": 6}
 ROPE_INVERSE, ROPE_INTERLEAVED = 1, 2
 
 
@@ -203,6 +205,27 @@ def bwd_xours(q, k, v, o, lse, d_o, cu_prefix, cu_suffix, group_sizes, total_pre
                                  workspace.numel(), _stream(torch, q.device))
     _check(st)
     return out
+
+
+def fwd_last(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, cu_prefix, cu_suffix, group_sizes, scale, out=None,
+             workspace=None):
+    """Final-token forward (pg_attn_fwd_last). Returns (o_last [n_suffixes, h_q, d], lse_last [h_q, n_suffixes])."""
+    import torch
+    ng, ns, tp, ts, hq, hkv, d = _shapes(q_pre, k_pre, q_suf, cu_prefix, cu_suffix, group_sizes)
+    dev = q_pre.device
+    if out is None:
+        out = (torch.empty((ns, hq, d), device=dev, dtype=q_pre.dtype),
+               torch.empty((hq, ns), device=dev, dtype=torch.float32))
+    if workspace is None:
+        nbytes = int(lib().pg_attn_fwd_last_workspace_size(ng, ns, tp, ts, hq, hkv, d))
+        workspace = torch.empty(nbytes, device=dev, dtype=torch.uint8)
+    o, lse = out
+    st = lib().pg_attn_fwd_last(_dtype_code(torch, q_pre.dtype), ng, ns, tp, ts, _ptr(cu_prefix), _ptr(cu_suffix),
+                                _ptr(group_sizes), hq, hkv, d, float(scale), _ptr(q_pre), _ptr(k_pre), _ptr(v_pre),
+                                _ptr(q_suf), _ptr(k_suf), _ptr(v_suf), _ptr(o), _ptr(lse), _ptr(workspace),
+                                workspace.numel(), _stream(torch, dev))
+    _check(st)
+    return o, lse
 
 
 def rope(q_pre, q_suf, k_pre, k_suf, cu_prefix, cu_suffix, group_sizes, base=10000.0, rotary_dim=None,

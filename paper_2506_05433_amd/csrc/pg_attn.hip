@@ -15,6 +15,7 @@
 #include "pg_bwd.hpp"
 #include "pg_fwd.hpp"
 #include "pg_plan.hpp"
+#include "pg_last.hpp"
 #include "pg_rope.hpp"
 
 namespace {
@@ -324,6 +325,35 @@ int bwd_impl(const Common& c, const int32_t* cu_p, const int32_t* cu_s, const in
   return PG_OK;
 }
 
+
+// ---------------------------------------------------------------- final-token forward
+struct LastLayout {
+  size_t hdr, ginfo, qoff, kvoff, blocks, nblk, part_o, part_ml, total;
+  int mpw, nb_max, nch;
+};
+
+LastLayout last_layout(int ng, int ns, int h_q, int h_kv, int d) {
+  LastLayout L{};
+  const int ratio = (h_kv > 0 && h_q >= h_kv) ? h_q / h_kv : 1;
+  L.mpw = ratio <= pg::kLastRows ? pg::kLastRows / ratio : 1;
+  L.nb_max = (int)std::min<long>(ns, ceil_div_l(ns, L.mpw) + ng);
+  const long units = (long)(L.nb_max > 0 ? L.nb_max : 1) * (h_kv > 0 ? h_kv : 1);
+  L.nch = (int)std::max<long>(1, std::min<long>(pg::kLastMaxChunks, ceil_div_l(1024, units)));
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
+  L.hdr = take(sizeof(pg::PlanHeader));
+  L.ginfo = take(sizeof(pg::GroupInfoEx) * (size_t)(ng > 0 ? ng : 1));
+  L.qoff = take(sizeof(int) * (size_t)(ng + 1));
+  L.kvoff = take(sizeof(int) * (size_t)(ng + 1));
+  L.blocks = take(sizeof(pg::LastBlock) * (size_t)(L.nb_max > 0 ? L.nb_max : 1));
+  L.nblk = take(sizeof(int));
+  const size_t slots = (size_t)(L.nb_max > 0 ? L.nb_max : 1) * (h_kv > 0 ? h_kv : 1) * L.nch * pg::kLastRows;
+  L.part_o = take(sizeof(float) * slots * (size_t)(d > 0 ? d : 1));
+  L.part_ml = take(sizeof(float) * slots * 2);
+  L.total = off;
+  return L;
+}
+
 // ---------------------------------------------------------------- rotary embedding
 // Workspace of the rope / positions calls: the planner's header and per-group ranges.
 struct RopeLayout {
@@ -514,6 +544,81 @@ int pg_timing_get(int kernel, int* launches, double* total_ms) {
   }
   *launches = cnt;
   *total_ms = tot;
+  return PG_OK;
+}
+
+size_t pg_attn_fwd_last_workspace_size(int n_groups, int n_suffixes, int total_prefix, int total_suffix, int h_q,
+                                       int h_kv, int head_dim) {
+  (void)total_prefix; (void)total_suffix;
+  if (n_groups < 0 || n_suffixes < 0 || total_prefix < 0 || total_suffix < 0 || h_q < 0 || h_kv < 0 ||
+      head_dim < 0)
+    return 0;
+  return last_layout(n_groups, n_suffixes, h_q, h_kv, head_dim).total;
+}
+
+int pg_attn_fwd_last(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                     const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                     int h_q, int h_kv, int head_dim, float softmax_scale,
+                     const void* q_pre, const void* k_pre, const void* v_pre,
+                     const void* q_suf, const void* k_suf, const void* v_suf,
+                     void* o_last, float* lse_last, void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  const Common c{dtype, n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, softmax_scale};
+  int rc = check_common(c, cu_prefix_lens, cu_suffix_lens, group_sizes);
+  if (rc) return rc;
+  if (h_q / h_kv > pg::kLastRows) return fail(PG_EUNSUPPORTED, "h_q / h_kv = %d exceeds %d", h_q / h_kv, pg::kLastRows);
+  if (total_prefix > 0 && (!q_pre || !k_pre || !v_pre)) return fail(PG_EINVAL, "a prefix tensor pointer is NULL");
+  if (total_suffix > 0 && (!q_suf || !k_suf || !v_suf)) return fail(PG_EINVAL, "a suffix tensor pointer is NULL");
+  if (n_suffixes > 0 && (!o_last || !lse_last)) return fail(PG_EINVAL, "o_last or lse_last is NULL");
+  const LastLayout L = last_layout(n_groups, n_suffixes, h_q, h_kv, head_dim);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(PG_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace_bytes, L.total);
+  if ((rc = device_ready())) return rc;
+  if (n_suffixes == 0) return PG_OK;
+  hipStream_t st = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  pg::LastArgs a{};
+  a.q_pre = q_pre; a.k_pre = k_pre; a.v_pre = v_pre; a.q_suf = q_suf; a.k_suf = k_suf; a.v_suf = v_suf;
+  a.o_last = o_last; a.lse_last = lse_last;
+  a.cu_s = cu_suffix_lens;
+  a.hdr = (const pg::PlanHeader*)(ws + L.hdr);
+  a.ginfo = (const pg::GroupInfoEx*)(ws + L.ginfo);
+  a.blocks = (const pg::LastBlock*)(ws + L.blocks);
+  a.n_blocks = (const int*)(ws + L.nblk);
+  a.part_o = (float*)(ws + L.part_o);
+  a.part_ml = (float*)(ws + L.part_ml);
+  a.h_q = h_q; a.h_kv = h_kv; a.ns = n_suffixes; a.nch = L.nch; a.nb_max = L.nb_max; a.mpw = L.mpw;
+  a.scale_log2 = softmax_scale * pg::kLog2e;
+  {
+    Timed tp(PG_K_PLAN, st);
+    const RopeLayout R{L.hdr, L.ginfo, L.qoff, L.kvoff, 0};
+    if ((rc = launch_rope_plan(R, ws, n_groups, n_suffixes, total_prefix, total_suffix, cu_prefix_lens,
+                               cu_suffix_lens, group_sizes, st)))
+      return rc;
+    hipLaunchKernelGGL(pg::plan_last_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, a.hdr, a.ginfo, n_groups, L.mpw,
+                       L.nb_max, (pg::LastBlock*)(ws + L.blocks), (int*)(ws + L.nblk));
+  }
+  const long blocks = pg::xcd_grid_blocks((long)L.nb_max * L.nch, h_kv, 1);
+  Timed tm(PG_K_LAST, st);
+  if (dtype == PG_BF16) {
+    if (head_dim == 128) {
+      hipLaunchKernelGGL((pg::last_kernel<pg::bf16, 128>), dim3((unsigned)blocks), dim3(pg::kLastThreads), 0, st, a);
+      hipLaunchKernelGGL((pg::last_merge_kernel<pg::bf16, 128>), dim3((unsigned)(L.nb_max * h_kv)), dim3(256), 0, st, a);
+    } else {
+      hipLaunchKernelGGL((pg::last_kernel<pg::bf16, 64>), dim3((unsigned)blocks), dim3(pg::kLastThreads), 0, st, a);
+      hipLaunchKernelGGL((pg::last_merge_kernel<pg::bf16, 64>), dim3((unsigned)(L.nb_max * h_kv)), dim3(256), 0, st, a);
+    }
+  } else {
+    if (head_dim == 128) {
+      hipLaunchKernelGGL((pg::last_kernel<float, 128>), dim3((unsigned)blocks), dim3(pg::kLastThreads), 0, st, a);
+      hipLaunchKernelGGL((pg::last_merge_kernel<float, 128>), dim3((unsigned)(L.nb_max * h_kv)), dim3(256), 0, st, a);
+    } else {
+      hipLaunchKernelGGL((pg::last_kernel<float, 64>), dim3((unsigned)blocks), dim3(pg::kLastThreads), 0, st, a);
+      hipLaunchKernelGGL((pg::last_merge_kernel<float, 64>), dim3((unsigned)(L.nb_max * h_kv)), dim3(256), 0, st, a);
+    }
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "final-token forward launch");
   return PG_OK;
 }
 

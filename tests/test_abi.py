@@ -151,3 +151,15 @@ def test_xours_validation():
     # a NULL tensor is rejected before launch; a short workspace too
     assert L.pg_attn_fwd_xours(0, 1, 2, 8, 6, p, p, p, 4, 2, 128, 0.125, p, p, None, p, p, p, 1 << 30, None) == 1
     assert L.pg_attn_bwd_xours(0, 1, 2, 8, 6, p, p, p, 4, 2, 128, 0.125, *[p] * 9, p, 16, None) == 3
+
+
+def test_last_validation_and_workspace():
+    L = binding.lib()
+    p = ctypes.c_void_p(256)
+    assert L.pg_attn_fwd_last_workspace_size(1, 16, 16384, 5000, 32, 8, 128) > 0
+    assert L.pg_attn_fwd_last_workspace_size(-1, 16, 0, 0, 32, 8, 128) == 0
+    # NULL output, bad head_dim, GQA ratio above 128, short workspace
+    assert L.pg_attn_fwd_last(0, 1, 2, 8, 6, p, p, p, 4, 2, 128, 0.125, *[p] * 6, None, p, p, 1 << 30, None) == 1
+    assert L.pg_attn_fwd_last(0, 1, 2, 8, 6, p, p, p, 4, 2, 96, 0.125, *[p] * 8, p, 1 << 30, None) == 2
+    assert L.pg_attn_fwd_last(0, 1, 2, 8, 6, p, p, p, 256, 1, 128, 0.125, *[p] * 8, p, 1 << 30, None) == 2
+    assert L.pg_attn_fwd_last(0, 1, 2, 8, 6, p, p, p, 4, 2, 128, 0.125, *[p] * 8, p, 16, None) == 3
