@@ -11,7 +11,6 @@ counted. The same kernels are also timed on the repeated-prefix layout
 (every member with its own copy of the prefix) for the speedup.
 """
 import argparse
-import glob
 import hashlib
 import json
 import os
@@ -187,10 +186,15 @@ def cpu_baseline(prob, useful_per_pair_head, budget_s):
             "seconds": round(dt, 2), "host_cpus": len(os.sched_getaffinity(0))}
 
 
+ATTN_SOURCES = ("pg_attn.hip", "pg_bwd.hpp", "pg_common.hpp", "pg_fwd.hpp", "pg_plan.hpp")
+
+
 def kernel_source_sha():
-    """Digest of the HIP sources: counter readings are only reported for the build they were taken on."""
+    """Digest of the sources the attention kernels and their launches are built from: counter readings are
+    only reported for the build they were taken on."""
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2506_05433_amd", "csrc", "*"))):
+    for name in ATTN_SOURCES:
+        f = os.path.join(ROOT, "paper_2506_05433_amd", "csrc", name)
         with open(f, "rb") as fh:
             h.update(os.path.basename(f).encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]

@@ -603,18 +603,18 @@ int pg_attn_fwd_last(int dtype, int n_groups, int n_suffixes, int total_prefix, 
   if (dtype == PG_BF16) {
     if (head_dim == 128) {
       hipLaunchKernelGGL((pg::last_kernel<pg::bf16, 128>), dim3((unsigned)blocks), dim3(pg::kLastThreads), 0, st, a);
-      hipLaunchKernelGGL((pg::last_merge_kernel<pg::bf16, 128>), dim3((unsigned)(L.nb_max * h_kv)), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((pg::last_merge_kernel<pg::bf16, 128>), dim3((unsigned)(4 * L.nb_max * h_kv)), dim3(256), 0, st, a);
     } else {
       hipLaunchKernelGGL((pg::last_kernel<pg::bf16, 64>), dim3((unsigned)blocks), dim3(pg::kLastThreads), 0, st, a);
-      hipLaunchKernelGGL((pg::last_merge_kernel<pg::bf16, 64>), dim3((unsigned)(L.nb_max * h_kv)), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((pg::last_merge_kernel<pg::bf16, 64>), dim3((unsigned)(4 * L.nb_max * h_kv)), dim3(256), 0, st, a);
     }
   } else {
     if (head_dim == 128) {
       hipLaunchKernelGGL((pg::last_kernel<float, 128>), dim3((unsigned)blocks), dim3(pg::kLastThreads), 0, st, a);
-      hipLaunchKernelGGL((pg::last_merge_kernel<float, 128>), dim3((unsigned)(L.nb_max * h_kv)), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((pg::last_merge_kernel<float, 128>), dim3((unsigned)(4 * L.nb_max * h_kv)), dim3(256), 0, st, a);
     } else {
       hipLaunchKernelGGL((pg::last_kernel<float, 64>), dim3((unsigned)blocks), dim3(pg::kLastThreads), 0, st, a);
-      hipLaunchKernelGGL((pg::last_merge_kernel<float, 64>), dim3((unsigned)(L.nb_max * h_kv)), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((pg::last_merge_kernel<float, 64>), dim3((unsigned)(4 * L.nb_max * h_kv)), dim3(256), 0, st, a);
     }
   }
   hipError_t e = hipGetLastError();

@@ -247,13 +247,16 @@ __global__ void __launch_bounds__(kLastThreads, 2) last_kernel(const LastArgs a)
 template <typename T, int D>
 __global__ void __launch_bounds__(256) last_merge_kernel(const LastArgs a) {
   __shared__ float s_w[kLastMaxChunks][kLastRows];  // weight of chunk c for row r: 2^(m_c - M) / L
-  const int b = blockIdx.x / a.h_kv, kvh = blockIdx.x - b * a.h_kv;
+  // one workgroup per (member block, kv head, quarter of the block's 128 rows)
+  const int quarter = blockIdx.x & 3, bk = blockIdx.x >> 2;
+  const int b = bk / a.h_kv, kvh = bk - b * a.h_kv;
   if (b >= *a.n_blocks) return;
   const LastBlock blk = a.blocks[b];
   const int ratio = a.h_q / a.h_kv;
-  const int rows = blk.m_count * ratio;
+  const int r0 = quarter * (kLastRows / 4);
+  const int rows = min(blk.m_count * ratio, r0 + kLastRows / 4);  // rows [r0, rows) of the block
   const size_t first = (size_t)(b * a.h_kv + kvh) * a.nch * kLastRows;  // slot row of chunk 0, row 0
-  for (int r = threadIdx.x; r < rows; r += 256) {
+  for (int r = r0 + threadIdx.x; r < rows; r += 256) {
     float M = -INFINITY;
     for (int ch = 0; ch < a.nch; ++ch) M = fmaxf(M, a.part_ml[2 * (first + (size_t)ch * kLastRows + r)]);
     float L = 0.f;
@@ -272,8 +275,8 @@ __global__ void __launch_bounds__(256) last_merge_kernel(const LastArgs a) {
   }
   __syncthreads();
   constexpr int Q = D / 4;  // float4 groups per row
-  for (int idx = threadIdx.x; idx < rows * Q; idx += 256) {
-    const int r = idx / Q, q = idx - r * Q;
+  for (int idx = threadIdx.x; idx < (rows - r0) * Q; idx += 256) {
+    const int r = r0 + idx / Q, q = idx % Q;
     f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int ch = 0; ch < a.nch; ++ch) {
       const size_t sr = first + (size_t)ch * kLastRows + r;

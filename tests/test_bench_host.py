@@ -49,17 +49,27 @@ def test_more_than_one_gpu_is_refused():
 
 
 def test_traffic_is_reported_only_for_the_profiled_sources(tmp_path, monkeypatch):
+    import shutil
+    shutil.copytree(os.path.join(bench.ROOT, "paper_2506_05433_amd", "csrc"),
+                    tmp_path / "paper_2506_05433_amd" / "csrc")
     prof = tmp_path / "profiles"
     prof.mkdir()
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     rec = dict(kernel="dkdv", workload="w", source_sha="not-this-build", copy_read_bytes=1 << 30,
                copy_write_bytes=1 << 30, copy_fetch_kib=524288.0, copy_write_kib=1048576.0, fetch_kib=1000.0,
                write_kib=10.0)
     (prof / "traffic_dkdv_w.json").write_text(json.dumps(rec))
-    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     assert bench.recorded_traffic("dkdv", "w") is None
-    rec["source_sha"] = bench.kernel_source_sha()
+    digest = bench.kernel_source_sha()
+    rec["source_sha"] = digest
     (prof / "traffic_dkdv_w.json").write_text(json.dumps(rec))
-    # the digest is taken over the package sources under ROOT; point it back at the repository
-    monkeypatch.setattr(bench, "kernel_source_sha", lambda: rec["source_sha"])
-    got = bench.recorded_traffic("dkdv", "w")
-    assert got == 1000.0 * 1024 * 2 + 10.0 * 1024 * 1
+    assert bench.recorded_traffic("dkdv", "w") == 1000.0 * 1024 * 2 + 10.0 * 1024 * 1
+    # sources the attention kernels are not built from do not invalidate the reading ...
+    with open(tmp_path / "paper_2506_05433_amd" / "csrc" / "pg_rope.hpp", "a") as fh:
+        fh.write("// edit\n")
+    assert bench.kernel_source_sha() == digest
+    # ... an edit of theirs does
+    with open(tmp_path / "paper_2506_05433_amd" / "csrc" / "pg_bwd.hpp", "a") as fh:
+        fh.write("// edit\n")
+    assert bench.kernel_source_sha() != digest
+    assert bench.recorded_traffic("dkdv", "w") is None
