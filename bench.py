@@ -7,8 +7,11 @@ resident in HBM). Prints ONE JSON line. ``value`` is useful TFLOP/s:
 4*d*H_q*pairs (forward) + 10*d*H_q*pairs (backward) per step, where pairs is
 the exact number of (query, key) pairs the grouped problem allows; masked
 work, ragged tiles and the repeated-prefix pairs the method avoids are not
-counted. The same kernels are also timed on the repeated-prefix layout
-(every member with its own copy of the prefix) for the speedup.
+counted. The timed step is the forward and backward calls captured once as a
+HIP graph and replayed (the eager time of the same calls is reported too;
+per-kernel times come from HIP events in the eager pass). The same kernels
+are also timed on the repeated-prefix layout (every member with its own copy
+of the prefix) for the speedup.
 """
 import argparse
 import hashlib
@@ -75,7 +78,27 @@ def time_steps(binding, torch, dev, bufs, steps, warmup):
     for k in ("plan", "fwd", "bwd_dot", "dkdv", "dq"):
         n, tot = binding.timing_get(k)
         kern[k] = {"launches": n, "avg_ms": (tot / n) if n else None}
-    return ms, kern
+    # the same step captured once as a HIP graph and replayed: no host launch cost per kernel
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_graph = e0.elapsed_time(e1) / steps
+    del graph
+    return ms_graph, kern, ms
 
 
 def alloc(binding, torch, dev, prob):
@@ -267,7 +290,7 @@ def main():
     bufs = alloc(binding, torch, dev, prob)
     print(f"[bench] {wl.name}: pairs={pairs} tokens={prob.total_prefix + prob.total_suffix}", file=sys.stderr,
           flush=True)
-    ms, kern = time_steps(binding, torch, dev, bufs, args.steps, args.warmup)
+    ms, kern, ms_eager = time_steps(binding, torch, dev, bufs, args.steps, args.warmup)
     value = (fwd_flops + bwd_flops) / (ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[prob.dtype]
     algo = {"fwd": fwd_flops, "dkdv": 8.0 * d * hq * pairs, "dq": 6.0 * d * hq * pairs}
@@ -282,6 +305,8 @@ def main():
         "config": {"workload": wl.name, "desc": wl.note, "n_groups": int(len(prob.prefix_lens)),
                    "total_prefix": prob.total_prefix, "total_suffix": prob.total_suffix, "h_q": hq,
                    "h_kv": prob.h_kv, "head_dim": d, "pairs": pairs, "parallelism": "single GPU"},
+        "ms_per_step_eager": round(ms_eager, 4), "step": "one HIP-graph replay of fwd+bwd (eager launches: "
+                                                         "ms_per_step_eager)",
         "pct_of_peak": round(100.0 * value / peak, 2),
         "fwd_tflops": round(fwd_flops / (fwd_ms * 1e-3) / 1e12, 2) if fwd_ms else None,
         "bwd_tflops": round(bwd_flops / (bwd_ms * 1e-3) / 1e12, 2) if bwd_ms else None,
@@ -298,7 +323,7 @@ def main():
         torch.cuda.empty_cache()
         rdev = binding.to_device(rep, "cuda")
         rbufs = alloc(binding, torch, rdev, rep)
-        rms, _ = time_steps(binding, torch, rdev, rbufs, args.steps, args.warmup)
+        rms, _, _ = time_steps(binding, torch, rdev, rbufs, args.steps, args.warmup)
         G = prob.group_sizes
         P = prob.prefix_lens
         sum_s = prob.suffix_lens.sum()
