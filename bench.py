@@ -253,6 +253,60 @@ def calibrate_copy(n_bytes):
     print(json.dumps({"copy_bytes": n_bytes, "launches": 3}))
 
 
+def tensor_bytes(prob, grads=True):
+    """Device bytes of the layer's tensors for one layout (inputs, outputs, LSE and, with grads, dO and dQ/dK/dV)."""
+    el = 2 if prob.dtype == "bf16" else 4
+    rows = prob.total_prefix + prob.total_suffix
+    per_row = (2 * prob.h_q + 2 * prob.h_kv) * prob.head_dim * el + prob.h_q * 4  # q, o, k, v, lse
+    if grads:
+        per_row += (2 * prob.h_q + 2 * prob.h_kv) * prob.head_dim * el  # do, dq, dk, dv
+    return rows * per_row
+
+
+def sweep(args):
+    """Fig. 2/3 grid of the paper: prefix 4096/8192/16384, G in {2,4,8,16}, prefix/response ratio r.
+
+    Every member has the same response length P / r (the setting of Appendix A.2). For each point the
+    grouped and the repeated layouts run the same kernels; the line reports both times, the speedup,
+    Eq. (17)'s attention-cost ratio, the useful TFLOP/s and the tensor + workspace bytes of both layouts.
+    """
+    import torch
+
+    from paper_2506_05433_amd import binding
+    from paper_2506_05433_amd.inputs import Workload, make_problem, repeated_layout
+    rows = []
+    for P in (4096, 8192, 16384):
+        for G in (2, 4, 8, 16):
+            for r in (1, 4, 16):
+                S = P // r
+                wl = Workload(f"sweep_P{P}_G{G}_r{r}", 1, G, ("fixed", P), ("uniform", S, S), 32, 8, 128, "bf16",
+                              1.0 / 128 ** 0.5)
+                prob = make_problem(wl, seed=0)
+                pairs = pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
+                flops = 14.0 * 128 * 32 * pairs
+                out = {"P": P, "G": G, "r": r, "S": S}
+                for name, pr in (("grouped", prob), ("repeated", repeated_layout(prob))):
+                    # names the case before any GPU work on it, on stdout
+                    print(f"[sweep] P={P} G={G} r={r} {name}: groups={len(pr.prefix_lens)} "
+                          f"total_prefix={pr.total_prefix} total_suffix={pr.total_suffix}", flush=True)
+                    dev = binding.to_device(pr, "cuda")
+                    bufs = alloc(binding, torch, dev, pr)
+                    ms, _, _ = time_steps(binding, torch, dev, bufs, args.steps, args.warmup)
+                    ws = sum(b.numel() for b in (bufs["ws_f"], bufs["ws_b"]))
+                    out[name + "_ms"] = round(ms, 4)
+                    out[name + "_MB"] = round((tensor_bytes(pr) + ws) / 1e6, 1)
+                    del dev, bufs
+                    torch.cuda.empty_cache()
+                eq17 = (P * P + G * S * (2 * P + S)) / (G * (P + S) ** 2)
+                out.update({"speedup": round(out["repeated_ms"] / out["grouped_ms"], 3),
+                            "eq17_cost_ratio": round(eq17, 4), "eq17_speedup": round(1 / eq17, 3),
+                            "useful_tflops": round(flops / (out["grouped_ms"] * 1e-3) / 1e12, 1),
+                            "memory_ratio": round(out["grouped_MB"] / out["repeated_MB"], 3)})
+                print(json.dumps(out), flush=True)
+                rows.append(out)
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -262,6 +316,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-repeated", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--sweep", action="store_true",
+                    help="run the paper's Fig. 2/3 grid (one JSON line per point) instead of the bench line")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES (counter calibration)")
     args = ap.parse_args()
@@ -272,6 +328,9 @@ def main():
 
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.sweep:
+        sweep(args)
         return
 
     import torch
