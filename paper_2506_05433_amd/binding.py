@@ -115,7 +115,37 @@ def _shapes(q_pre, k_pre, q_suf, cu_prefix, cu_suffix, group_sizes):
     for t in (cu_prefix, cu_suffix, group_sizes):
         if t.dtype.itemsize != 4 or t.dtype.is_floating_point or not t.is_contiguous():
             raise TypeError("grouping arrays must be contiguous int32 device tensors")
+    if q_pre.dim() != 3 or q_suf.dim() != 3 or k_pre.dim() != 3:
+        raise ValueError("q and k tensors must be [rows, heads, head_dim]")
     return n_groups, n_suffixes, q_pre.shape[0], q_suf.shape[0], q_pre.shape[1], k_pre.shape[1], q_pre.shape[2]
+
+
+def _expect(device, dtype, **tensors):
+    """Every named tensor is (shape, tensor): contiguous, of that shape, dtype (None: float32) and device.
+
+    The library receives raw pointers, so a strided view, a wrong shape or a tensor on another device would
+    be read or written out of place; they are rejected here instead."""
+    import torch
+    for name, (shape, t) in tensors.items():
+        want = torch.float32 if dtype is None or name.startswith("lse") else dtype
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{name} must be a tensor")
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+        if t.dtype != want:
+            raise TypeError(f"{name} has dtype {t.dtype}, expected {want}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if t.device != device:
+            raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if device.type != "cuda":
+        raise ValueError(f"tensors must be GPU device memory, got {device}")
+
+
+def _workspace(t, device):
+    import torch
+    if t.dtype != torch.uint8 or not t.is_contiguous() or t.device != device:
+        raise ValueError("workspace must be a contiguous uint8 tensor on the tensors' device")
 
 
 def fwd(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, cu_prefix, cu_suffix, group_sizes, scale,
@@ -123,7 +153,7 @@ def fwd(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, cu_prefix, cu_suffix, group_si
     """Grouped attention forward. Returns (o_pre, o_suf, lse_pre, lse_suf)."""
     import torch
     ng, ns, tp, ts, hq, hkv, d = _shapes(q_pre, k_pre, q_suf, cu_prefix, cu_suffix, group_sizes)
-    dev = q_pre.device
+    dev, dt = q_pre.device, q_pre.dtype
     if out is None:
         out = (torch.empty_like(q_pre), torch.empty_like(q_suf),
                torch.empty((hq, tp), device=dev, dtype=torch.float32),
@@ -132,6 +162,11 @@ def fwd(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, cu_prefix, cu_suffix, group_si
     if workspace is None:
         workspace = torch.empty(need, device=dev, dtype=torch.uint8)
     o_pre, o_suf, lse_pre, lse_suf = out
+    _expect(dev, dt, q_pre=((tp, hq, d), q_pre), k_pre=((tp, hkv, d), k_pre), v_pre=((tp, hkv, d), v_pre),
+            q_suf=((ts, hq, d), q_suf), k_suf=((ts, hkv, d), k_suf), v_suf=((ts, hkv, d), v_suf),
+            o_pre=((tp, hq, d), o_pre), o_suf=((ts, hq, d), o_suf), lse_pre=((hq, tp), lse_pre),
+            lse_suf=((hq, ts), lse_suf))
+    _workspace(workspace, dev)
     st = lib().pg_attn_fwd(
         _dtype_code(torch, q_pre.dtype), ng, ns, tp, ts,
         _ptr(cu_prefix), _ptr(cu_suffix), _ptr(group_sizes), hq, hkv, d, float(scale),
@@ -147,13 +182,20 @@ def bwd(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, o_pre, o_suf, lse_pre, lse_suf
     """Grouped attention backward. Returns (dq_pre, dk_pre, dv_pre, dq_suf, dk_suf, dv_suf)."""
     import torch
     ng, ns, tp, ts, hq, hkv, d = _shapes(q_pre, k_pre, q_suf, cu_prefix, cu_suffix, group_sizes)
-    dev = q_pre.device
+    dev, dt = q_pre.device, q_pre.dtype
     if out is None:
         out = (torch.empty_like(q_pre), torch.empty_like(k_pre), torch.empty_like(v_pre),
                torch.empty_like(q_suf), torch.empty_like(k_suf), torch.empty_like(v_suf))
     need = workspace_bytes("bwd", ng, ns, tp, ts, hq, hkv, d)
     if workspace is None:
         workspace = torch.empty(need, device=dev, dtype=torch.uint8)
+    pre_q, pre_kv, suf_q, suf_kv = (tp, hq, d), (tp, hkv, d), (ts, hq, d), (ts, hkv, d)
+    _expect(dev, dt, q_pre=(pre_q, q_pre), k_pre=(pre_kv, k_pre), v_pre=(pre_kv, v_pre), q_suf=(suf_q, q_suf),
+            k_suf=(suf_kv, k_suf), v_suf=(suf_kv, v_suf), o_pre=(pre_q, o_pre), o_suf=(suf_q, o_suf),
+            lse_pre=((hq, tp), lse_pre), lse_suf=((hq, ts), lse_suf), do_pre=(pre_q, do_pre),
+            do_suf=(suf_q, do_suf), dq_pre=(pre_q, out[0]), dk_pre=(pre_kv, out[1]), dv_pre=(pre_kv, out[2]),
+            dq_suf=(suf_q, out[3]), dk_suf=(suf_kv, out[4]), dv_suf=(suf_kv, out[5]))
+    _workspace(workspace, dev)
     st = lib().pg_attn_bwd(
         _dtype_code(torch, q_pre.dtype), ng, ns, tp, ts,
         _ptr(cu_prefix), _ptr(cu_suffix), _ptr(group_sizes), hq, hkv, d, float(scale),
@@ -179,6 +221,9 @@ def fwd_xours(q, k, v, cu_prefix, cu_suffix, group_sizes, total_prefix, scale, o
         workspace = torch.empty(workspace_bytes("fwd", ng, ns, tp, ts, hq, hkv, d), device=q.device,
                                 dtype=torch.uint8)
     o, lse = out
+    _expect(q.device, q.dtype, q=((rows, hq, d), q), k=((rows, hkv, d), k), v=((rows, hkv, d), v),
+            o=((rows, hq, d), o), lse=((hq, rows), lse))
+    _workspace(workspace, q.device)
     st = lib().pg_attn_fwd_xours(_dtype_code(torch, q.dtype), ng, ns, tp, ts, _ptr(cu_prefix), _ptr(cu_suffix),
                                  _ptr(group_sizes), hq, hkv, d, float(scale), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
                                  _ptr(lse), _ptr(workspace), workspace.numel(), _stream(torch, q.device))
@@ -199,6 +244,10 @@ def bwd_xours(q, k, v, o, lse, d_o, cu_prefix, cu_suffix, group_sizes, total_pre
     if workspace is None:
         workspace = torch.empty(workspace_bytes("bwd", ng, ns, tp, ts, hq, hkv, d), device=q.device,
                                 dtype=torch.uint8)
+    _expect(q.device, q.dtype, q=((rows, hq, d), q), k=((rows, hkv, d), k), v=((rows, hkv, d), v),
+            o=((rows, hq, d), o), lse=((hq, rows), lse), d_o=((rows, hq, d), d_o), dq=((rows, hq, d), out[0]),
+            dk=((rows, hkv, d), out[1]), dv=((rows, hkv, d), out[2]))
+    _workspace(workspace, q.device)
     st = lib().pg_attn_bwd_xours(_dtype_code(torch, q.dtype), ng, ns, tp, ts, _ptr(cu_prefix), _ptr(cu_suffix),
                                  _ptr(group_sizes), hq, hkv, d, float(scale), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
                                  _ptr(lse), _ptr(d_o), *[_ptr(t) for t in out], _ptr(workspace),
@@ -220,6 +269,10 @@ def fwd_last(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, cu_prefix, cu_suffix, gro
         nbytes = int(lib().pg_attn_fwd_last_workspace_size(ng, ns, tp, ts, hq, hkv, d))
         workspace = torch.empty(nbytes, device=dev, dtype=torch.uint8)
     o, lse = out
+    _expect(dev, q_pre.dtype, q_pre=((tp, hq, d), q_pre), k_pre=((tp, hkv, d), k_pre), v_pre=((tp, hkv, d), v_pre),
+            q_suf=((ts, hq, d), q_suf), k_suf=((ts, hkv, d), k_suf), v_suf=((ts, hkv, d), v_suf),
+            o_last=((ns, hq, d), o), lse_last=((hq, ns), lse))
+    _workspace(workspace, dev)
     st = lib().pg_attn_fwd_last(_dtype_code(torch, q_pre.dtype), ng, ns, tp, ts, _ptr(cu_prefix), _ptr(cu_suffix),
                                 _ptr(group_sizes), hq, hkv, d, float(scale), _ptr(q_pre), _ptr(k_pre), _ptr(v_pre),
                                 _ptr(q_suf), _ptr(k_suf), _ptr(v_suf), _ptr(o), _ptr(lse), _ptr(workspace),
@@ -246,6 +299,14 @@ def rope(q_pre, q_suf, k_pre, k_suf, cu_prefix, cu_suffix, group_sizes, base=100
         out = tuple(None if t is None else torch.empty_like(t) for t in ins)
     if workspace is None:
         workspace = torch.empty(int(lib().pg_rope_workspace_size(ng)), device=ref.device, dtype=torch.uint8)
+    named = {}
+    for name, t, o, rows_, h in (("q_pre", q_pre, out[0], tp, hq), ("q_suf", q_suf, out[1], ts, hq),
+                                 ("k_pre", k_pre, out[2], tp, hkv), ("k_suf", k_suf, out[3], ts, hkv)):
+        if t is not None:
+            named[name] = ((rows_, h, d), t)
+            named[name + "_out"] = ((rows_, h, d), o)
+    _expect(ref.device, ref.dtype, **named)
+    _workspace(workspace, ref.device)
     flags = (ROPE_INVERSE if inverse else 0) | (ROPE_INTERLEAVED if interleaved else 0)
     st = lib().pg_rope(_dtype_code(torch, ref.dtype), ng, ns, tp, ts, _ptr(cu_prefix), _ptr(cu_suffix),
                        _ptr(group_sizes), hq, hkv, d, d if rotary_dim is None else int(rotary_dim), float(base),
