@@ -406,7 +406,9 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
   constexpr int BN = kDqBN;
   constexpr int KK = D / 16, DB = D / 32;
   constexpr int TILE = LdsTile<T, D>::bytes(BN);
-  __shared__ __attribute__((aligned(16))) char smem[2][2][TILE];  // [buffer][K, V]
+  // two K/V buffers as distinct LDS objects, named statically by a loop unrolled by two
+  // (the forward kernel explains why)
+  __shared__ __attribute__((aligned(16))) char sK0[TILE], sV0[TILE], sK1[TILE], sV1[TILE];
 
   const BlockSlot slot = xcd_slot(blockIdx.x, a.h_q, a.h_q / a.h_kv);
   const int rank = slot.unit, head = slot.head;
@@ -462,13 +464,13 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
   ldv.init(kvstride, wave, lane);
   FragOffsets<T, D> fo;
   fo.init(lane);
-  auto issue = [&](int j) {
+  auto issue = [&](int j, char* kdst, char* vdst) {
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
     const size_t kx = (size_t)(k0 + (segA ? xo_pre : xo_suf));
-    ldk.load(smem[j & 1][0], (segA ? Kp : Ks) + kx * kvstride + kvh * D, kvstride, kend - k0);
-    ldv.load(smem[j & 1][1], (segA ? Vp : Vs) + kx * kvstride + kvh * D, kvstride, kend - k0);
+    ldk.load(kdst, (segA ? Kp : Ks) + kx * kvstride + kvh * D, kvstride, kend - k0);
+    ldv.load(vdst, (segA ? Vp : Vs) + kx * kvstride + kvh * D, kvstride, kend - k0);
   };
 
   f32x16 acc[DB];
@@ -476,17 +478,9 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
   for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
   const float c = a.scale_log2;
 
-  if (ntiles > 0) {
-    issue(0);
-    ldk.store(smem[0][0]);
-    ldv.store(smem[0][1]);
-  }
-  ldk.wait();
-  __syncthreads();
-
-  for (int j = 0; j < ntiles; ++j) {
-    const int buf = j & 1;
-    if (j + 1 < ntiles) issue(j + 1);
+  // one key tile: start the copy of tile j + 1 into (Kn, Vn), work on (Kt, Vt), publish
+  auto step = [&](int j, const char* Kt, const char* Vt, char* Kn, char* Vn) {
+    if (j + 1 < ntiles) issue(j + 1, Kn, Vn);
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
@@ -502,8 +496,6 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
       if (!segA) full = full && (k0 >= seg_w_hi);
     }
     if (wave_active && !skip) {
-      const char* Kt = smem[buf][0];
-      const char* Vt = smem[buf][1];
       // two blocks of 32 keys, one after the other
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
@@ -542,11 +534,23 @@ __global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const 
       }
     }
     if (j + 1 < ntiles) {
-      ldk.store(smem[buf ^ 1][0]);
-      ldv.store(smem[buf ^ 1][1]);
+      ldk.store(Kn);
+      ldv.store(Vn);
     }
     ldk.wait();
     __syncthreads();
+  };
+
+  if (ntiles > 0) {
+    issue(0, sK0, sV0);
+    ldk.store(sK0);
+    ldv.store(sV0);
+  }
+  ldk.wait();
+  __syncthreads();
+  for (int j = 0; j < ntiles; j += 2) {
+    step(j, sK0, sV0, sK1, sV1);
+    if (j + 1 < ntiles) step(j + 1, sK1, sV1, sK0, sV0);
   }
 
   if (!wave_active || !qvalid) return;

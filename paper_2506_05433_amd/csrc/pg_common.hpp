@@ -146,12 +146,6 @@ struct Elt<bf16> {
   __device__ __forceinline__ static f32x16 mma(const Frag& a, const Frag& b, const f32x16& c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
-  // Same product with the accumulator pinned to AGPRs. Long-lived accumulators of
-  // kernels that run one wave per SIMD stay in the accumulator file this way instead
-  // of being copied between register files around every instruction.
-  __device__ __forceinline__ static void mma_acc(f32x16& c, const Frag& a, const Frag& b) {
-    asm("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
-  }
   // the 8 elements [8*half8, 8*half8+8) of row `row` (one 16-byte chunk)
   template <int D>
   __device__ __forceinline__ static Frag lds_row(const char* tile, int row, int chunk) {
@@ -215,7 +209,6 @@ struct Elt<float> {
     for (int s = 0; s < 8; ++s) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a.v[s], b.v[s], c, 0, 0, 0);
     return c;
   }
-  __device__ __forceinline__ static void mma_acc(f32x16& c, const Frag& a, const Frag& b) { c = mma(a, b, c); }
   template <int D>
   __device__ __forceinline__ static Frag lds_row(const char* tile, int row, int chunk) {
     // `chunk` counts 8-element groups (32 bytes for fp32)

@@ -51,7 +51,11 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
   constexpr int KK = D / 16;  // k steps over head_dim
   constexpr int DB = D / 32;  // 32-wide blocks of head_dim
   constexpr int TILE = LdsTile<T, D>::bytes(BN);
-  __shared__ __attribute__((aligned(16))) char smem[2][2][TILE];  // [buffer][K, V]
+  // Two K/V buffers as four distinct LDS objects: the loop below is unrolled by two so
+  // that every access names its buffer statically, which lets the compiler see that the
+  // copy into one buffer cannot overlap the reads of the other (with one array indexed
+  // by j & 1 it has to wait for the copy to land before the first read of the tile).
+  __shared__ __attribute__((aligned(16))) char sK0[TILE], sV0[TILE], sK1[TILE], sV1[TILE];
 
   const BlockSlot slot = xcd_slot(blockIdx.x, a.h_q, a.h_q / a.h_kv);
   const int rank = slot.unit, head = slot.head;
@@ -100,15 +104,15 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
   ldv.init(kvstride, wave, lane);
   FragOffsets<T, D> fo;
   fo.init(lane);
-  auto issue = [&](int j) {
+  auto issue = [&](int j, char* kdst, char* vdst) {
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
     const size_t kx = (size_t)(k0 + (segA ? xo_pre : xo_suf));
     const T* kb = (segA ? Kp : Ks) + kx * kvstride + kvh * D;
     const T* vb = (segA ? Vp : Vs) + kx * kvstride + kvh * D;
-    ldk.load(smem[j & 1][0], kb, kvstride, kend - k0);
-    ldv.load(smem[j & 1][1], vb, kvstride, kend - k0);
+    ldk.load(kdst, kb, kvstride, kend - k0);
+    ldv.load(vdst, vb, kvstride, kend - k0);
   };
 
   f32x16 acc_o[DB];
@@ -117,17 +121,9 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
   float m_run = -INFINITY, l_run = 0.f;
   const float c = a.scale_log2;
 
-  if (ntiles > 0) {
-    issue(0);
-    ldk.store(smem[0][0]);
-    ldv.store(smem[0][1]);
-  }
-  ldk.wait();
-  __syncthreads();
-
-  for (int j = 0; j < ntiles; ++j) {
-    const int buf = j & 1;
-    if (j + 1 < ntiles) issue(j + 1);
+  // one key tile: start the copy of tile j + 1 into (Kn, Vn), work on (Kt, Vt), publish
+  auto step = [&](int j, const char* Kt, const char* Vt, char* Kn, char* Vn) {
+    if (j + 1 < ntiles) issue(j + 1, Kn, Vn);
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
@@ -145,8 +141,6 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
       if (!segA) full = full && (k0 >= seg_w_hi);
     }
     if (wave_active && !skip) {
-      const char* Kt = smem[buf][0];
-      const char* Vt = smem[buf][1];
       f32x16 s[2];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
@@ -214,11 +208,23 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
       }
     }
     if (j + 1 < ntiles) {
-      ldk.store(smem[buf ^ 1][0]);
-      ldv.store(smem[buf ^ 1][1]);
+      ldk.store(Kn);
+      ldv.store(Vn);
     }
     ldk.wait();
     __syncthreads();
+  };
+
+  if (ntiles > 0) {
+    issue(0, sK0, sV0);
+    ldk.store(sK0);
+    ldv.store(sV0);
+  }
+  ldk.wait();
+  __syncthreads();
+  for (int j = 0; j < ntiles; j += 2) {
+    step(j, sK0, sV0, sK1, sV1);
+    if (j + 1 < ntiles) step(j + 1, sK1, sV1, sK0, sV0);
   }
 
   if (!wave_active) return;
