@@ -191,11 +191,16 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     }
   };
 
-  Stager<T, BQ, D, kKvThreads> ldq, ldo;
+  // Query tiles are staged through registers (16 per thread), not copied straight into
+  // LDS: with the three buffers in one LDS array indexed at run time, a direct copy into
+  // one of them would make every read of another wait for the copy to land.
+  TileLoader<T, BQ, D, kKvThreads> ldq, ldo;
   ldq.init(a.h_q * D, wave, lane);
   ldo.init(a.h_q * D, wave, lane);
   FragOffsets<T, D> fo;
   fo.init(lane);
+  // per-row values of the next tile: loaded with its copies, used only in commit() (a use
+  // right after the load would wait for the copies issued before it as well)
   float pf_lse = 0.f, pf_dsum = 0.f;
   int pf_seg = 0;
   auto issue = [&](const TileInfo& ti, int it) {  // `it` selects the buffer
@@ -205,19 +210,23 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     ldq.load(smem[it % NBUF][0], Qs + off, a.h_q * D, ti.qend - ti.q0);
     ldo.load(smem[it % NBUF][1], Gs + off, a.h_q * D, ti.qend - ti.q0);
     if (tid < BQ) {
-      const int q = ti.q0 + tid;
-      const bool v = q < ti.qend;
+      const int q = min(ti.q0 + tid, ti.qend - 1);  // padding rows read the last row; commit() drops them
       const float* L = ti.qsuf ? a.lse_suf : a.lse_pre;
       const int ld = ti.qsuf ? lse_ld_suf : lse_ld_pre;
-      pf_lse = v ? L[(size_t)ti.hq * ld + q + (ti.qsuf ? xo_suf : xo_pre)] * kLog2e : INFINITY;
-      pf_dsum = v ? a.dsum[(size_t)ti.hq * rows_all + (ti.qsuf ? a.total_prefix : 0) + q] : 0.f;
-      pf_seg = (v && ti.qsuf) ? a.seg_start[q] : 0;
+      pf_lse = L[(size_t)ti.hq * ld + q + (ti.qsuf ? xo_suf : xo_pre)];
+      pf_dsum = a.dsum[(size_t)ti.hq * rows_all + (ti.qsuf ? a.total_prefix : 0) + q];
+      if (ti.qsuf) pf_seg = a.seg_start[q];
     }
   };
-  auto commit = [&](int buf) {
+  auto commit = [&](const TileInfo& ti, int buf) {
     ldq.store(smem[buf][0]);
     ldo.store(smem[buf][1]);
-    if (tid < BQ) { s_lse[buf][tid] = pf_lse; s_dsum[buf][tid] = pf_dsum; s_seg[buf][tid] = pf_seg; }
+    if (tid < BQ) {
+      const bool v = ti.q0 + tid < ti.qend;
+      s_lse[buf][tid] = v ? pf_lse * kLog2e : INFINITY;  // padding rows: P = 0
+      s_dsum[buf][tid] = v ? pf_dsum : 0.f;
+      s_seg[buf][tid] = (v && ti.qsuf) ? pf_seg : 0;
+    }
   };
 
   // The walk: every wave stages its share of tile it+1, works on its tile, and meets the
@@ -227,7 +236,7 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
   auto walk_tiles = [&](auto&& work) {
     int cur_hd = it0 / (per_head > 0 ? per_head : 1), cur_j = it0 - cur_hd * per_head;
     TileInfo ti_cur = info(cur_hd, cur_j), ti_prev = ti_cur;  // tiles it and it - 1
-    if (it1 > it0) { issue(ti_cur, it0 % NBUF); commit(it0 % NBUF); }
+    if (it1 > it0) { issue(ti_cur, it0 % NBUF); commit(ti_cur, it0 % NBUF); }
     ldq.wait();
     __syncthreads();
     for (int it = it0; it <= it1; ++it) {
@@ -236,7 +245,7 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
       const TileInfo ti_next = info(nxt_hd, nxt_j);
       if (it + 1 < it1) issue(ti_next, it + 1);
       work(it, ti_cur, ti_prev);
-      if (it + 1 < it1) commit((it + 1) % NBUF);
+      if (it + 1 < it1) commit(ti_next, (it + 1) % NBUF);
       ti_prev = ti_cur;
       ti_cur = ti_next;
       cur_hd = nxt_hd;

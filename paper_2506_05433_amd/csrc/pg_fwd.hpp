@@ -104,15 +104,22 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
   ldv.init(kvstride, wave, lane);
   FragOffsets<T, D> fo;
   fo.init(lane);
-  auto issue = [&](int j, char* kdst, char* vdst) {
+  // source rows of key tile j: (pointer to its first row of this kv head, valid rows)
+  auto tile_src = [&](int j, const T* pre, const T* suf, int& rows) {
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
-    const int kend = segA ? kA1 : kB1;
-    const size_t kx = (size_t)(k0 + (segA ? xo_pre : xo_suf));
-    const T* kb = (segA ? Kp : Ks) + kx * kvstride + kvh * D;
-    const T* vb = (segA ? Vp : Vs) + kx * kvstride + kvh * D;
-    ldk.load(kdst, kb, kvstride, kend - k0);
-    ldv.load(vdst, vb, kvstride, kend - k0);
+    rows = (segA ? kA1 : kB1) - k0;
+    return (segA ? pre : suf) + (size_t)(k0 + (segA ? xo_pre : xo_suf)) * kvstride + kvh * D;
+  };
+  auto issue_k = [&](int j, char* kdst) {
+    int rows;
+    const T* src = tile_src(j, Kp, Ks, rows);
+    ldk.load(kdst, src, kvstride, rows);
+  };
+  auto issue_v = [&](int j, char* vdst) {
+    int rows;
+    const T* src = tile_src(j, Vp, Vs, rows);
+    ldv.load(vdst, src, kvstride, rows);
   };
 
   f32x16 acc_o[DB];
@@ -121,9 +128,74 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
   float m_run = -INFINITY, l_run = 0.f;
   const float c = a.scale_log2;
 
-  // one key tile: start the copy of tile j + 1 into (Kn, Vn), work on (Kt, Vt), publish
+  // S^T = K Q^T for one 64-key tile
+  auto s_product = [&](const char* Kt, f32x16 (&s)[2]) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      s[kb] = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) s[kb] = E::mma(fo.row(Kt, 32 * kb, kk), qf[kk], s[kb]);
+    }
+  };
+  // Lazy running max of one tile's (masked) scores: a row keeps its max until a tile
+  // exceeds it by more than 2^8, so most tiles need no rescale of O and l (p <= 256 is
+  // harmless in fp32/bf16; the log-sum-exp is exact for any choice of m).
+  auto tile_max = [&](const f32x16 (&s)[2]) {
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
+    tmax = wave_swap32_max(tmax) * c;  // c > 0: max(c*s) = c*max(s)
+    const float m_new = (tmax > m_run + 8.f) ? tmax : m_run;
+    if (__any(m_new != m_run)) {
+      const float alpha = fast_exp2(m_run - ((m_new == -INFINITY) ? 0.f : m_new));
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) acc_o[db] *= alpha;
+    }
+    m_run = m_new;
+  };
+  // P = exp2(S*c - m) against the row's current max, l += rowsum(P), O^T += V^T P^T
+  auto exp_pv = [&](f32x16 (&s)[2], const char* Vt) {
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = fast_exp2(fmaf(s[kb][r], c, -m_use));
+        s[kb][r] = p;
+        psum += p;
+      }
+    }
+    l_run += psum;
+    Frag pf[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) pf[t] = E::acc_to_frag(s[t >> 1], t & 1);
+    // O^T += V^T P^T over the 64 keys (4 k steps of 16)
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int db = 0; db < DB; ++db) acc_o[db] = E::mma(fo.tr(Vt, t, db), pf[t], acc_o[db]);
+  };
+
+  // Tiles [0, nfull) are visible to every row of the workgroup (no mask, no skip): the
+  // dense prefix of a response tile, and the prefix keys left of a prefix tile's
+  // diagonal. They run software-pipelined: iteration j computes the scores of tile j + 1
+  // while it exponentiates those of tile j and adds P V, with no branch in between, so
+  // each wave interleaves matrix and vector instructions instead of alternating between
+  // them (both waves of a SIMD meet at every barrier, so they would otherwise run the same
+  // phase at the same time); the max of tile j + 1 and the rare rescale follow. K runs two
+  // tiles ahead of V: iteration j reads K(j + 1) and V(j) and copies K(j + 2), V(j + 1).
+  // The arithmetic is the same, in the same order, as for a boundary tile.
+  const int nfull = suffix ? (kA1 - kA0) / BN : (td.row0 - kA0 + 1) / BN;
+  // the remaining tiles: per-wave skip and masks at the boundaries
   auto step = [&](int j, const char* Kt, const char* Vt, char* Kn, char* Vn) {
-    if (j + 1 < ntiles) issue(j + 1, Kn, Vn);
+    if (j + 1 < ntiles) {
+      issue_k(j + 1, Kn);
+      issue_v(j + 1, Vn);
+    }
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
@@ -142,13 +214,7 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
     }
     if (wave_active && !skip) {
       f32x16 s[2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        s[kb] = f32x16{};
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk)
-          s[kb] = E::mma(fo.row(Kt, 32 * kb, kk), qf[kk], s[kb]);
-      }
+      s_product(Kt, s);
       // Mask, only on tiles that straddle a boundary (a real branch: the empty asm keeps
       // the compiler from turning it into selects executed on every tile). Key offset
       // o = 32kb + 8(r/4) + r%4 of register r is a compile-time constant; the lane's
@@ -167,45 +233,8 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
             s[kb][r] = ((o >= lo) & (o < hi)) ? s[kb][r] : -INFINITY;
           }
       }
-      float tmax = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, s[kb][r]);
-      tmax = wave_swap32_max(tmax) * c;  // c > 0: max(c*s) = c*max(s)
-      // Lazy running max: a row keeps its max until a tile exceeds it by more than
-      // 2^8, so most tiles need no rescale of O (p <= 256 is harmless in fp32/bf16;
-      // the log-sum-exp is exact for any choice of m).
-      const float m_new = (tmax > m_run + 8.f) ? tmax : m_run;
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      float psum = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(fmaf(s[kb][r], c, -m_use));
-          s[kb][r] = p;
-          psum += p;
-        }
-      }
-      if (__any(m_new != m_run)) {
-        const float alpha = fast_exp2(m_run - m_use);
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) acc_o[db] *= alpha;
-      }
-      l_run += psum;
-      m_run = m_new;
-      // O^T += V^T P^T over the 64 keys (4 k steps of 16)
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const Frag pf = E::acc_to_frag(s[t >> 1], t & 1);
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const Frag vf = fo.tr(Vt, t, db);
-          acc_o[db] = E::mma(vf, pf, acc_o[db]);
-        }
-      }
+      tile_max(s);
+      exp_pv(s, Vt);
     }
     if (j + 1 < ntiles) {
       ldk.store(Kn);
@@ -214,17 +243,51 @@ __global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(con
     ldk.wait();
     __syncthreads();
   };
+  auto pipe_step = [&](int j, f32x16 (&s_cur)[2], f32x16 (&s_nxt)[2], const char* Kt1, const char* Vt,
+                       char* Kn2, char* Vn1) {
+    const bool k2 = j + 2 <= nfull && j + 2 < ntiles, v1 = j + 1 < ntiles;
+    if (k2) issue_k(j + 2, Kn2);
+    if (v1) issue_v(j + 1, Vn1);
+    if (wave_active) {
+      // the scores of tile j + 1 (unused when j + 1 == nfull: the buffer then holds an
+      // earlier tile or nothing, and the boundary loop recomputes them)
+      s_product(Kt1, s_nxt);
+      exp_pv(s_cur, Vt);
+      if (j + 1 < nfull) tile_max(s_nxt);
+    }
+    if (k2) ldk.store(Kn2);
+    if (v1) ldv.store(Vn1);
+    ldk.wait();
+    __syncthreads();
+  };
 
   if (ntiles > 0) {
-    issue(0, sK0, sV0);
+    issue_k(0, sK0);
+    issue_v(0, sV0);
     ldk.store(sK0);
     ldv.store(sV0);
   }
   ldk.wait();
   __syncthreads();
-  for (int j = 0; j < ntiles; j += 2) {
-    step(j, sK0, sV0, sK1, sV1);
-    if (j + 1 < ntiles) step(j + 1, sK1, sV1, sK0, sV0);
+  if (nfull > 0) {
+    f32x16 sa[2], sb[2];
+    const bool k1 = 1 < ntiles;
+    if (k1) issue_k(1, sK1);
+    if (wave_active) {
+      s_product(sK0, sa);
+      tile_max(sa);
+    }
+    if (k1) ldk.store(sK1);
+    ldk.wait();
+    __syncthreads();
+    for (int j = 0; j < nfull; j += 2) {
+      pipe_step(j, sa, sb, sK1, sV0, sK0, sV1);
+      if (j + 1 < nfull) pipe_step(j + 1, sb, sa, sK0, sV1, sK1, sV0);
+    }
+  }
+  for (int j = nfull; j < ntiles; ++j) {
+    const bool odd = j & 1;
+    step(j, odd ? sK1 : sK0, odd ? sV1 : sV0, odd ? sK0 : sK1, odd ? sV0 : sV1);
   }
 
   if (!wave_active) return;
