@@ -51,6 +51,11 @@ def repeated_pair_count(prefix_lens, group_sizes, suffix_lens):
     return total
 
 
+def progress(msg):
+    """A progress line on stderr (the JSON result is the only stdout line)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def time_steps(binding, torch, dev, bufs, steps, warmup):
     def step():
         binding.fwd(dev["q_pre"], dev["k_pre"], dev["v_pre"], dev["q_suf"], dev["k_suf"], dev["v_suf"],
@@ -339,6 +344,7 @@ def main():
     from paper_2506_05433_amd.inputs import WORKLOADS, make_problem, repeated_layout
 
     wl = WORKLOADS[args.workload]
+    progress(f"{wl.name}: generating inputs")
     prob = make_problem(wl, seed=0)
     d, hq = prob.head_dim, prob.h_q
     pairs = pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
@@ -350,6 +356,7 @@ def main():
     print(f"[bench] {wl.name}: pairs={pairs} tokens={prob.total_prefix + prob.total_suffix}", file=sys.stderr,
           flush=True)
     ms, kern, ms_eager = time_steps(binding, torch, dev, bufs, args.steps, args.warmup)
+    progress(f"grouped layout: {ms:.3f} ms/step")
     value = (fwd_flops + bwd_flops) / (ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[prob.dtype]
     algo = {"fwd": fwd_flops, "dkdv": 8.0 * d * hq * pairs, "dq": 6.0 * d * hq * pairs}
@@ -377,12 +384,14 @@ def main():
     out["rope"] = time_rope(binding, torch, dev, prob, args.steps, args.warmup)
     out["last"] = time_last(binding, torch, dev, prob, args.steps, args.warmup)
     if not args.no_repeated:
+        progress("building the repeated-prefix layout")
         rep = repeated_layout(prob)
         del dev, bufs
         torch.cuda.empty_cache()
         rdev = binding.to_device(rep, "cuda")
         rbufs = alloc(binding, torch, rdev, rep)
         rms, _, _ = time_steps(binding, torch, rdev, rbufs, args.steps, args.warmup)
+        progress(f"repeated layout: {rms:.3f} ms/step")
         G = prob.group_sizes
         P = prob.prefix_lens
         sum_s = prob.suffix_lens.sum()
@@ -391,6 +400,7 @@ def main():
                     "speedup_target": round(target, 3), "speedup_ceiling_pairs": round(rep_pairs / pairs, 3)})
         del rdev, rbufs
     if not args.no_cpu_baseline:
+        progress("timing the CPU oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(prob, 14.0 * d, args.cpu_budget)
     print(json.dumps(out))
 
