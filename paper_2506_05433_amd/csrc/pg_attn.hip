@@ -599,22 +599,26 @@ int pg_attn_fwd_last(int dtype, int n_groups, int n_suffixes, int total_prefix, 
                        L.nb_max, (pg::LastBlock*)(ws + L.blocks), (int*)(ws + L.nblk));
   }
   const long blocks = pg::xcd_grid_blocks((long)L.nb_max * L.nch, h_kv, 1);
+  const long merge = (long)(head_dim == 128 ? pg::merge_groups<128>() : pg::merge_groups<64>()) * L.nb_max * h_kv;
+  if (blocks > INT32_MAX || merge > INT32_MAX)
+    return fail(PG_EUNSUPPORTED, "%d responses x %d kv heads exceed the launch grid", n_suffixes, h_kv);
+  const dim3 gc((unsigned)blocks), gm((unsigned)merge), tc(pg::kLastThreads), tm_(pg::kMergeThreads);
   Timed tm(PG_K_LAST, st);
   if (dtype == PG_BF16) {
     if (head_dim == 128) {
-      hipLaunchKernelGGL((pg::last_kernel<pg::bf16, 128>), dim3((unsigned)blocks), dim3(pg::kLastThreads), 0, st, a);
-      hipLaunchKernelGGL((pg::last_merge_kernel<pg::bf16, 128>), dim3((unsigned)(4 * L.nb_max * h_kv)), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((pg::last_kernel<pg::bf16, 128>), gc, tc, 0, st, a);
+      hipLaunchKernelGGL((pg::last_merge_kernel<pg::bf16, 128>), gm, tm_, 0, st, a);
     } else {
-      hipLaunchKernelGGL((pg::last_kernel<pg::bf16, 64>), dim3((unsigned)blocks), dim3(pg::kLastThreads), 0, st, a);
-      hipLaunchKernelGGL((pg::last_merge_kernel<pg::bf16, 64>), dim3((unsigned)(4 * L.nb_max * h_kv)), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((pg::last_kernel<pg::bf16, 64>), gc, tc, 0, st, a);
+      hipLaunchKernelGGL((pg::last_merge_kernel<pg::bf16, 64>), gm, tm_, 0, st, a);
     }
   } else {
     if (head_dim == 128) {
-      hipLaunchKernelGGL((pg::last_kernel<float, 128>), dim3((unsigned)blocks), dim3(pg::kLastThreads), 0, st, a);
-      hipLaunchKernelGGL((pg::last_merge_kernel<float, 128>), dim3((unsigned)(4 * L.nb_max * h_kv)), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((pg::last_kernel<float, 128>), gc, tc, 0, st, a);
+      hipLaunchKernelGGL((pg::last_merge_kernel<float, 128>), gm, tm_, 0, st, a);
     } else {
-      hipLaunchKernelGGL((pg::last_kernel<float, 64>), dim3((unsigned)blocks), dim3(pg::kLastThreads), 0, st, a);
-      hipLaunchKernelGGL((pg::last_merge_kernel<float, 64>), dim3((unsigned)(4 * L.nb_max * h_kv)), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((pg::last_kernel<float, 64>), gc, tc, 0, st, a);
+      hipLaunchKernelGGL((pg::last_merge_kernel<float, 64>), gm, tm_, 0, st, a);
     }
   }
   hipError_t e = hipGetLastError();

@@ -83,7 +83,9 @@ __global__ void __launch_bounds__(kLastThreads, 2) last_kernel(const LastArgs a)
   constexpr int BN = 64;
   constexpr int KK = D / 16, DB = D / 32;
   constexpr int TILE = LdsTile<T, D>::bytes(BN);
-  __shared__ __attribute__((aligned(16))) char smem[2][2][TILE];  // [buffer][K, V]
+  // two K/V buffers as distinct LDS objects, named statically by a loop unrolled by two (a
+  // copy into one buffer then never makes reads of the other wait for it)
+  __shared__ __attribute__((aligned(16))) char sK0[TILE], sV0[TILE], sK1[TILE], sV1[TILE];
 
   const BlockSlot slot = xcd_slot(blockIdx.x, a.h_kv, 1);
   const int unit = slot.unit, kvh = slot.head;
@@ -130,12 +132,12 @@ __global__ void __launch_bounds__(kLastThreads, 2) last_kernel(const LastArgs a)
   ldv.init(kvstride, wave, lane);
   FragOffsets<T, D> fo;
   fo.init(lane);
-  auto issue = [&](int j) {
+  auto issue = [&](int j, char* kdst, char* vdst) {
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
-    ldk.load(smem[j & 1][0], (segA ? Kp : Ks) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0);
-    ldv.load(smem[j & 1][1], (segA ? Vp : Vs) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0);
+    ldk.load(kdst, (segA ? Kp : Ks) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0);
+    ldv.load(vdst, (segA ? Vp : Vs) + (size_t)k0 * kvstride + kvh * D, kvstride, kend - k0);
   };
 
   f32x16 acc_o[DB];
@@ -144,24 +146,15 @@ __global__ void __launch_bounds__(kLastThreads, 2) last_kernel(const LastArgs a)
   float m_run = -INFINITY, l_run = 0.f;
   const float c = a.scale_log2;
 
-  if (j1 > j0) {
-    issue(j0);
-    ldk.store(smem[j0 & 1][0]);
-    ldv.store(smem[j0 & 1][1]);
-  }
-  ldk.wait();
-  __syncthreads();
-  for (int j = j0; j < j1; ++j) {
-    const int buf = j & 1;
-    if (j + 1 < j1) issue(j + 1);
+  // one key tile: start the copy of tile j + 1 into (Kn, Vn), work on (Kt, Vt), publish
+  auto step = [&](int j, const char* Kt, const char* Vt, char* Kn, char* Vn) {
+    if (j + 1 < j1) issue(j + 1, Kn, Vn);
     const bool segA = j < nA;
     const int k0 = segA ? kA0 + j * BN : kB0 + (j - nA) * BN;
     const int kend = segA ? kA1 : kB1;
     const bool skip = !segA && (k0 >= whi || k0 + BN <= wlo);
     const bool full = segA && (k0 + BN <= kend);
     if (wave_active && !skip) {
-      const char* Kt = smem[buf][0];
-      const char* Vt = smem[buf][1];
       f32x16 s[2];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
@@ -217,11 +210,23 @@ __global__ void __launch_bounds__(kLastThreads, 2) last_kernel(const LastArgs a)
       }
     }
     if (j + 1 < j1) {
-      ldk.store(smem[buf ^ 1][0]);
-      ldv.store(smem[buf ^ 1][1]);
+      ldk.store(Kn);
+      ldv.store(Vn);
     }
     ldk.wait();
     __syncthreads();
+  };
+
+  if (j1 > j0) {
+    issue(j0, sK0, sV0);
+    ldk.store(sK0);
+    ldv.store(sV0);
+  }
+  ldk.wait();
+  __syncthreads();
+  for (int j = j0; j < j1; j += 2) {
+    step(j, sK0, sV0, sK1, sV1);
+    if (j + 1 < j1) step(j + 1, sK1, sV1, sK0, sV0);
   }
 
   if (!rvalid) return;
@@ -244,47 +249,56 @@ __global__ void __launch_bounds__(kLastThreads, 2) last_kernel(const LastArgs a)
 // Combines the chunks of one (member block, kv head) in chunk order and writes o_last and
 // lse_last: with M the largest chunk max, o = sum_c 2^(m_c - M) o_c / sum_c 2^(m_c - M) l_c.
 // A row whose sequence is empty (no prefix, no response) gets o = 0 and lse = -inf.
+// One thread per (row, 4 output columns), kMergeThreads / (D/4) rows per workgroup, so the
+// merge of even a single member block spreads over hundreds of workgroups; the threads of a
+// row each recompute its (M, L) from the same cached chunk states.
+constexpr int kMergeThreads = 128;
+template <int D>
+constexpr int merge_groups() { return kLastRows / (kMergeThreads / (D / 4)); }  // row groups per block
+
 template <typename T, int D>
-__global__ void __launch_bounds__(256) last_merge_kernel(const LastArgs a) {
-  __shared__ float s_w[kLastMaxChunks][kLastRows];  // weight of chunk c for row r: 2^(m_c - M) / L
-  // one workgroup per (member block, kv head, quarter of the block's 128 rows)
-  const int quarter = blockIdx.x & 3, bk = blockIdx.x >> 2;
+__global__ void __launch_bounds__(kMergeThreads) last_merge_kernel(const LastArgs a) {
+  constexpr int Q = D / 4;                 // float4 groups per row
+  constexpr int RPW = kMergeThreads / Q;   // rows per workgroup
+  constexpr int G = merge_groups<D>();
+  const int bk = blockIdx.x / G, rg = blockIdx.x - bk * G;
   const int b = bk / a.h_kv, kvh = bk - b * a.h_kv;
   if (b >= *a.n_blocks) return;
   const LastBlock blk = a.blocks[b];
   const int ratio = a.h_q / a.h_kv;
-  const int r0 = quarter * (kLastRows / 4);
-  const int rows = min(blk.m_count * ratio, r0 + kLastRows / 4);  // rows [r0, rows) of the block
-  const size_t first = (size_t)(b * a.h_kv + kvh) * a.nch * kLastRows;  // slot row of chunk 0, row 0
-  for (int r = r0 + threadIdx.x; r < rows; r += 256) {
-    float M = -INFINITY;
-    for (int ch = 0; ch < a.nch; ++ch) M = fmaxf(M, a.part_ml[2 * (first + (size_t)ch * kLastRows + r)]);
-    float L = 0.f;
-    if (M != -INFINITY)
-      for (int ch = 0; ch < a.nch; ++ch) {
-        const size_t sr = first + (size_t)ch * kLastRows + r;
-        L += a.part_ml[2 * sr + 1] * fast_exp2(a.part_ml[2 * sr] - M);
-      }
-    const float inv = (M == -INFINITY) ? 0.f : 1.f / L;
-    for (int ch = 0; ch < a.nch; ++ch) {
-      const size_t sr = first + (size_t)ch * kLastRows + r;
-      s_w[ch][r] = (M == -INFINITY) ? 0.f : fast_exp2(a.part_ml[2 * sr] - M) * inv;
-    }
-    const int member = blk.m_first + r / ratio, head = kvh * ratio + r % ratio;
-    a.lse_last[(size_t)head * a.ns + member] = (M == -INFINITY) ? -INFINITY : (M + fast_log2(L)) * kLn2;
+  const int r = rg * RPW + (int)threadIdx.x / Q, q = (int)threadIdx.x % Q;
+  if (r >= blk.m_count * ratio) return;
+  const size_t first = (size_t)(b * a.h_kv + kvh) * a.nch * kLastRows + r;  // slot row of chunk 0
+  // Every chunk's state and output block is loaded up front (the loops run over the fixed
+  // maximum with clamped indices, so all loads are in flight together); chunks past nch get
+  // max -inf and weight 0, which leaves the sums unchanged.
+  const int last = a.nch - 1;
+  float mc[kLastMaxChunks], lc[kLastMaxChunks];
+#pragma unroll
+  for (int ch = 0; ch < kLastMaxChunks; ++ch) {
+    const size_t sr = first + (size_t)min(ch, last) * kLastRows;
+    mc[ch] = ch <= last ? a.part_ml[2 * sr] : -INFINITY;
+    lc[ch] = a.part_ml[2 * sr + 1];
   }
-  __syncthreads();
-  constexpr int Q = D / 4;  // float4 groups per row
-  for (int idx = threadIdx.x; idx < (rows - r0) * Q; idx += 256) {
-    const int r = r0 + idx / Q, q = idx % Q;
-    f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int ch = 0; ch < a.nch; ++ch) {
-      const size_t sr = first + (size_t)ch * kLastRows + r;
-      o += s_w[ch][r] * *(const f32x4*)(a.part_o + sr * D + 4 * q);
-    }
-    const int member = blk.m_first + r / ratio, head = kvh * ratio + r % ratio;
-    Elt<T>::store4((T*)a.o_last + ((size_t)member * a.h_q + head) * D + 4 * q, o[0], o[1], o[2], o[3]);
+  float M = -INFINITY;
+#pragma unroll
+  for (int ch = 0; ch < kLastMaxChunks; ++ch) M = fmaxf(M, mc[ch]);
+  float L = 0.f;
+  if (M != -INFINITY) {
+#pragma unroll
+    for (int ch = 0; ch < kLastMaxChunks; ++ch) L += lc[ch] * fast_exp2(mc[ch] - M);
   }
+  const float inv = (M == -INFINITY) ? 0.f : 1.f / L;
+  f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ch = 0; ch < kLastMaxChunks; ++ch) {
+    const size_t sr = first + (size_t)min(ch, last) * kLastRows;
+    const float w = (M == -INFINITY) ? 0.f : fast_exp2(mc[ch] - M) * inv;
+    o += w * *(const f32x4*)(a.part_o + sr * D + 4 * q);
+  }
+  const int member = blk.m_first + r / ratio, head = kvh * ratio + r % ratio;
+  Elt<T>::store4((T*)a.o_last + ((size_t)member * a.h_q + head) * D + 4 * q, o[0], o[1], o[2], o[3]);
+  if (q == 0) a.lse_last[(size_t)head * a.ns + member] = (M == -INFINITY) ? -INFINITY : (M + fast_log2(L)) * kLn2;
 }
 
 }  // namespace pg
