@@ -46,12 +46,14 @@ struct Layout {
 };
 
 // Pieces each prefix key tile's query walk is split into for the dK/dV kernel: enough
-// workgroups to balance the long prefix walks over the CUs (about 1024 prefix pieces),
-// at most 8, and 1 when there are already that many prefix key tiles.
+// workgroups to balance the long prefix walks over the CUs (about 512 prefix pieces, i.e.
+// two per CU), at most 8, and 1 when there are already that many prefix key tiles. More
+// pieces balance better but each adds a full fp32 partial to write and reduce; measured on
+// the single-group and large-group workloads, 512 beats 256 and 1024-4096.
 int kv_chunks_for(int ng, int tp, int h_kv) {
   if (tp <= 0 || h_kv <= 0) return 1;
   const long tiles = (ceil_div_l(tp, pg::kKvBN) + ng) * (long)h_kv;
-  const long c = ceil_div_l(1024, tiles);
+  const long c = ceil_div_l(512, tiles);
   return (int)(c < 1 ? 1 : (c > 8 ? 8 : c));
 }
 
