@@ -73,7 +73,8 @@ __global__ void __launch_bounds__(256) bwd_dot_kernel(const BwdArgs a) {
 // Each wave therefore holds one kv operand and one accumulator (about half the
 // registers of a wave doing all four products), so two waves fit per SIMD and one's
 // exp/VALU work overlaps the other's matrix instructions. Query tiles are
-// triple-buffered in LDS (P-waves read tile i, G-waves tile i-1, tile i+1 loads).
+// triple-buffered in LDS (P-waves read tile i, G-waves tile i-1, tile i+1 loads through
+// registers and is written to LDS after the work on tile i).
 #ifndef PG_KV_GROUPS
 #define PG_KV_GROUPS 4
 #endif

@@ -12,7 +12,9 @@
 // Per 64-key tile, each wave computes S^T = K Q^T (keys x queries) so that every
 // lane owns one query column: the running max/sum of a row live in one lane pair
 // (l, l^32). P^T is then directly the B operand of O^T += V^T P^T; V^T comes from
-// the row-major LDS tile through transposing reads.
+// the row-major LDS tile through transposing reads. The leading tiles that every row
+// of the workgroup sees run software-pipelined (the scores of tile j+1 are computed
+// next to the exponentials of tile j); the rest take the masked path.
 #pragma once
 #include "pg_common.hpp"
 #include "pg_plan.hpp"
