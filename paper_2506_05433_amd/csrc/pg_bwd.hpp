@@ -75,19 +75,13 @@ __global__ void __launch_bounds__(256) bwd_dot_kernel(const BwdArgs a) {
 // exp/VALU work overlaps the other's matrix instructions. Query tiles are
 // triple-buffered in LDS (P-waves read tile i, G-waves tile i-1, tile i+1 loads through
 // registers and is written to LDS after the work on tile i).
-#ifndef PG_KV_GROUPS
-#define PG_KV_GROUPS 4
-#endif
-constexpr int kKvGroups = PG_KV_GROUPS;      // 32-key groups per workgroup
+constexpr int kKvGroups = 4;                 // 32-key groups per workgroup
 constexpr int kKvBN = 32 * kKvGroups;        // keys per workgroup
 constexpr int kKvThreads = 128 * kKvGroups;  // a P-wave and a G-wave per key group
 
-#ifndef PG_KV_BQ_BF16
-#define PG_KV_BQ_BF16 64
-#endif
 template <typename T>
-struct KvTileRows {
-  static constexpr int value = sizeof(T) == 2 ? PG_KV_BQ_BF16 : 32;
+struct KvTileRows {  // query rows per staged tile
+  static constexpr int value = sizeof(T) == 2 ? 64 : 32;
 };
 
 template <typename T, int D>
@@ -268,9 +262,6 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
         const char* Gt = smem[buf][1];
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
-#ifdef PG_KV_SCHED_BARRIER
-          __builtin_amdgcn_sched_barrier(0);
-#endif
           f32x16 sc = f32x16{};
 #pragma unroll
           for (int kk = 0; kk < KK; ++kk)
@@ -324,9 +315,6 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
         const char* Gt = smem[buf][1];
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
-#ifdef PG_KV_SCHED_BARRIER
-          __builtin_amdgcn_sched_barrier(0);
-#endif
           f32x16 dp = f32x16{};
 #pragma unroll
           for (int kk = 0; kk < KK; ++kk)
@@ -407,10 +395,7 @@ constexpr int kDqBN = 64;
 constexpr int kDqThreads = 256;
 
 template <typename T, int D>
-#ifndef PG_DQ_MIN_BLOCKS
-#define PG_DQ_MIN_BLOCKS 2
-#endif
-__global__ void __launch_bounds__(kDqThreads, PG_DQ_MIN_BLOCKS) dq_kernel(const BwdArgs a) {
+__global__ void __launch_bounds__(kDqThreads, 2) dq_kernel(const BwdArgs a) {
   using E = Elt<T>;
   using Frag = typename E::Frag;
   constexpr int BN = kDqBN;

@@ -43,10 +43,7 @@ constexpr int kFwdBN = 64;   // keys per tile
 constexpr int kFwdThreads = 256;
 
 template <typename T, int D>
-#ifndef PG_FWD_MIN_BLOCKS
-#define PG_FWD_MIN_BLOCKS 2
-#endif
-__global__ void __launch_bounds__(kFwdThreads, PG_FWD_MIN_BLOCKS) fwd_kernel(const FwdArgs a) {
+__global__ void __launch_bounds__(kFwdThreads, 2) fwd_kernel(const FwdArgs a) {
   using E = Elt<T>;
   using Frag = typename E::Frag;
   constexpr int BN = kFwdBN;
