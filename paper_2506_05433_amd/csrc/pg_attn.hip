@@ -166,6 +166,27 @@ bool debug_validate() {
   return v && v[0] == '1';
 }
 
+// PG_PLAN_MULTI=1 runs the multi-kernel planner even where the one-block planner applies
+// (the two must give the same plan; a test compares them).
+bool plan_multi() {
+  const char* v = getenv("PG_PLAN_MULTI");
+  return v && v[0] == '1';
+}
+
+// Launch check after the planner, and the PG_DEBUG_VALIDATE readback of its verdict.
+int finish_plan(const pg::PlanHeader* hdr, hipStream_t st) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "planner launch");
+  if (debug_validate()) {
+    pg::PlanHeader h;
+    e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "PG_DEBUG_VALIDATE readback");
+    if (h.error) return fail(PG_EINVAL, "grouping arrays are inconsistent (checked on the device)");
+  }
+  return PG_OK;
+}
+
 // Runs the planner kernels. `bwd` also builds the key/value tile list.
 int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p, const int32_t* cu_s,
                 const int32_t* gsz, hipStream_t st, bool bwd, bool xl) {
@@ -174,6 +195,15 @@ int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p,
   auto* gi = (pg::GroupInfoEx*)(ws + L.ginfo);
   int* qoff = (int*)(ws + L.qoff);
   int* kvoff = (int*)(ws + L.kvoff);
+  if (L.max_q <= pg::kPlanThreads && (!bwd || L.max_kv <= pg::kPlanThreads) && !plan_multi()) {
+    // every tile list fits one block: the whole planner in one launch
+    hipLaunchKernelGGL(pg::plan_fused_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, cu_p, cu_s, gsz, c.ng, c.ns,
+                       c.tp, c.ts, pg::kFwdBM, pg::kKvBN, L.kv_chunks, L.max_q, bwd ? L.max_kv : 0x7fffffffL, hdr, gi,
+                       qoff, kvoff, (pg::TileDesc*)(ws + L.qtiles), (int*)(ws + L.qorder),
+                       bwd ? (pg::TileDesc*)(ws + L.kvtiles) : nullptr, (int*)(ws + L.kvorder), (int*)(ws + L.seg),
+                       (bwd && xl) ? (int*)(ws + L.xrow) : nullptr);
+    return finish_plan(hdr, st);
+  }
   hipLaunchKernelGGL(pg::plan_groups_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, cu_p, cu_s, gsz, c.ng, c.ns,
                      c.tp, c.ts, pg::kFwdBM, pg::kKvBN, L.kv_chunks, L.max_q, bwd ? L.max_kv : 0x7fffffffL, hdr, gi, qoff,
                      kvoff);
@@ -201,16 +231,7 @@ int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p,
     hipLaunchKernelGGL(pg::xrow_kernel, dim3((unsigned)ceil_div_l((long)c.tp + c.ts, 256)), dim3(256), 0, st, cu_p,
                        cu_s, c.ng, c.ns, c.tp, c.ts, hdr, gi, (int*)(ws + L.xrow));
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return hip_fail(e, "planner launch");
-  if (debug_validate()) {
-    pg::PlanHeader h;
-    e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, st);
-    if (e == hipSuccess) e = hipStreamSynchronize(st);
-    if (e != hipSuccess) return hip_fail(e, "PG_DEBUG_VALIDATE readback");
-    if (h.error) return fail(PG_EINVAL, "grouping arrays are inconsistent (checked on the device)");
-  }
-  return PG_OK;
+  return finish_plan(hdr, st);
 }
 
 template <typename T, int D>
@@ -393,16 +414,7 @@ int launch_rope_plan(const RopeLayout& L, char* ws, int ng, int ns, int tp, int 
   hipLaunchKernelGGL(pg::plan_groups_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, cu_p, cu_s, gsz, ng, ns, tp,
                      ts, pg::kFwdBM, pg::kKvBN, 1, 0x7fffffffL, 0x7fffffffL, hdr, (pg::GroupInfoEx*)(ws + L.ginfo),
                      (int*)(ws + L.qoff), (int*)(ws + L.kvoff));
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return hip_fail(e, "planner launch");
-  if (debug_validate()) {
-    pg::PlanHeader h;
-    e = hipMemcpyAsync(&h, hdr, sizeof(h), hipMemcpyDeviceToHost, st);
-    if (e == hipSuccess) e = hipStreamSynchronize(st);
-    if (e != hipSuccess) return hip_fail(e, "PG_DEBUG_VALIDATE readback");
-    if (h.error) return fail(PG_EINVAL, "grouping arrays are inconsistent (checked on the device)");
-  }
-  return PG_OK;
+  return finish_plan(hdr, st);
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }

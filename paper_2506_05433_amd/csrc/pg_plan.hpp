@@ -54,14 +54,21 @@ __device__ __forceinline__ int upper_index(const int* a, int lo, int hi, int x) 
 
 constexpr int kPlanThreads = 1024;
 
-// One block. Validates and computes per-group ranges and tile offsets.
-__global__ void __launch_bounds__(kPlanThreads) plan_groups_kernel(
-    const int* __restrict__ cu_p, const int* __restrict__ cu_s, const int* __restrict__ gsz,
-    int ng, int ns, int tp, int ts, int bm, int bkv, int kv_chunks, long max_q, long max_kv,
-    PlanHeader* hdr, GroupInfoEx* ginfo, int* qoff, int* kvoff) {
-  __shared__ int tmp[kPlanThreads];
-  __shared__ int err;
-  __shared__ int carry[3];
+// Shared memory of the one-block planner steps.
+struct PlanShared {
+  int tmp[kPlanThreads];
+  int err;
+  int carry[3];
+};
+
+// One block of kPlanThreads threads. Validates and computes per-group ranges and tile offsets.
+__device__ inline void plan_groups_body(const int* __restrict__ cu_p, const int* __restrict__ cu_s,
+                                        const int* __restrict__ gsz, int ng, int ns, int tp, int ts, int bm, int bkv,
+                                        int kv_chunks, long max_q, long max_kv, PlanHeader* hdr, GroupInfoEx* ginfo,
+                                        int* qoff, int* kvoff, PlanShared& sh) {
+  int* tmp = sh.tmp;
+  int& err = sh.err;
+  int* carry = sh.carry;
   const int t = threadIdx.x;
   if (t == 0) { err = 0; carry[0] = carry[1] = carry[2] = 0; }
   __syncthreads();
@@ -127,13 +134,18 @@ __global__ void __launch_bounds__(kPlanThreads) plan_groups_kernel(
   }
 }
 
-// One thread per (possible) tile: fills the descriptors. `which` 0 = query tiles, 1 = kv tiles.
-__global__ void plan_tiles_kernel(const int* __restrict__ cu_s, int ng, int bm, int bkv, int kv_chunks, int max_tiles,
-                                  const PlanHeader* hdr, const GroupInfoEx* __restrict__ ginfo,
-                                  const int* __restrict__ off, TileDesc* tiles, int which) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  const int n = which ? hdr->n_kvtiles : hdr->n_qtiles;
-  if (i >= n || i >= max_tiles) return;
+__global__ void __launch_bounds__(kPlanThreads) plan_groups_kernel(
+    const int* __restrict__ cu_p, const int* __restrict__ cu_s, const int* __restrict__ gsz,
+    int ng, int ns, int tp, int ts, int bm, int bkv, int kv_chunks, long max_q, long max_kv,
+    PlanHeader* hdr, GroupInfoEx* ginfo, int* qoff, int* kvoff) {
+  __shared__ PlanShared sh;
+  plan_groups_body(cu_p, cu_s, gsz, ng, ns, tp, ts, bm, bkv, kv_chunks, max_q, max_kv, hdr, ginfo, qoff, kvoff, sh);
+}
+
+// Descriptor of tile i (< the number of tiles). `which` 0 = query tiles, 1 = kv tiles.
+__device__ inline void plan_tile(int i, const int* __restrict__ cu_s, int ng, int bm, int bkv, int kv_chunks,
+                                 const GroupInfoEx* __restrict__ ginfo, const int* __restrict__ off, TileDesc* tiles,
+                                 int which) {
   const int g = upper_index(off, 0, ng, i);  // off[ng] == n > i, groups with no tile share offsets
   // skip groups with zero tiles that share the offset of the next one
   const GroupInfoEx gi = ginfo[g];
@@ -176,6 +188,16 @@ __global__ void plan_tiles_kernel(const int* __restrict__ cu_s, int ng, int bm, 
   tiles[i] = d;
 }
 
+// One thread per (possible) tile: fills the descriptors.
+__global__ void plan_tiles_kernel(const int* __restrict__ cu_s, int ng, int bm, int bkv, int kv_chunks, int max_tiles,
+                                  const PlanHeader* hdr, const GroupInfoEx* __restrict__ ginfo,
+                                  const int* __restrict__ off, TileDesc* tiles, int which) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int n = which ? hdr->n_kvtiles : hdr->n_qtiles;
+  if (i >= n || i >= max_tiles) return;
+  plan_tile(i, cu_s, ng, bm, bkv, kv_chunks, ginfo, off, tiles, which);
+}
+
 // Longest-first order: order[rank] = tile, rank by (work desc, index asc). Deterministic.
 __global__ void __launch_bounds__(256) plan_rank_kernel(const PlanHeader* hdr, const TileDesc* __restrict__ tiles,
                                                         int* order, int which) {
@@ -205,18 +227,15 @@ __global__ void seg_start_kernel(const int* __restrict__ cu_s, int ns, int ts, c
                                  int* seg_start) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= ts || hdr->error) return;
-  const int m = upper_index(cu_s, 0, ns, r);
-  seg_start[r] = cu_s[m];
+  seg_start[r] = cu_s[upper_index(cu_s, 0, ns, r)];
 }
 
 // Row map of the single-buffer layout of Eq. (2) (per group [P; R_1; ...; R_G], groups
 // one after another): xrow[t] for packed prefix row t, xrow[total_prefix + s] for packed
 // response row s. Prefix row t of group g is preceded by the responses of the earlier
 // groups (s0 of g rows); response row s of group g by the prefixes of groups 0..g (p1).
-__global__ void xrow_kernel(const int* __restrict__ cu_p, const int* __restrict__ cu_s, int ng, int ns, int tp,
-                            int ts, const PlanHeader* hdr, const GroupInfoEx* __restrict__ ginfo, int* xrow) {
-  const int row = blockIdx.x * blockDim.x + threadIdx.x;
-  if (row >= tp + ts || hdr->error) return;
+__device__ inline void xrow_of(int row, const int* __restrict__ cu_p, const int* __restrict__ cu_s, int ng, int ns,
+                               int tp, const GroupInfoEx* __restrict__ ginfo, int* xrow) {
   if (row < tp) {
     const int g = upper_index(cu_p, 0, ng, row);
     xrow[row] = row + ginfo[g].s0;
@@ -230,6 +249,54 @@ __global__ void xrow_kernel(const int* __restrict__ cu_p, const int* __restrict_
     if (ginfo[mid].m0 <= m) lo = mid; else hi = mid;
   }
   xrow[row] = s + ginfo[lo].p1;
+}
+
+__global__ void xrow_kernel(const int* __restrict__ cu_p, const int* __restrict__ cu_s, int ng, int ns, int tp,
+                            int ts, const PlanHeader* hdr, const GroupInfoEx* __restrict__ ginfo, int* xrow) {
+  const int row = blockIdx.x * blockDim.x + threadIdx.x;
+  if (row >= tp + ts || hdr->error) return;
+  xrow_of(row, cu_p, cu_s, ng, ns, tp, ginfo, xrow);
+}
+
+// The whole planner in one block, for plans whose tile lists each fit in kPlanThreads
+// entries (the host checks the bounds): the steps above in order, separated by block
+// barriers instead of kernel boundaries, with the same results. Saves the launch and
+// memory latency of four to six dependent one-block kernels per call.
+__global__ void __launch_bounds__(kPlanThreads) plan_fused_kernel(
+    const int* __restrict__ cu_p, const int* __restrict__ cu_s, const int* __restrict__ gsz, int ng, int ns, int tp,
+    int ts, int bm, int bkv, int kv_chunks, long max_q, long max_kv, PlanHeader* hdr, GroupInfoEx* ginfo, int* qoff,
+    int* kvoff, TileDesc* qtiles, int* qorder, TileDesc* kvtiles, int* kvorder, int* seg_start, int* xrow) {
+  __shared__ PlanShared sh;
+  plan_groups_body(cu_p, cu_s, gsz, ng, ns, tp, ts, bm, bkv, kv_chunks, max_q, max_kv, hdr, ginfo, qoff, kvoff, sh);
+  __syncthreads();
+  const int t = threadIdx.x;
+  const int error = hdr->error;
+  const int nq = hdr->n_qtiles, nkv = kvtiles ? hdr->n_kvtiles : 0;  // both <= kPlanThreads (host bound)
+  if (t < nq) plan_tile(t, cu_s, ng, bm, bkv, 1, ginfo, qoff, qtiles, 0);
+  if (t < nkv) plan_tile(t, cu_s, ng, bm, bkv, kv_chunks, ginfo, kvoff, kvtiles, 1);
+  __syncthreads();
+  // longest-first ranks, the rule of plan_rank_kernel: (work desc, index asc)
+  for (int which = 0; which < 2; ++which) {
+    const int n = which ? nkv : nq;
+    const TileDesc* tiles = which ? kvtiles : qtiles;
+    int* order = which ? kvorder : qorder;
+    sh.tmp[t] = t < n ? tiles[t].work : -1;
+    __syncthreads();
+    if (t < n) {
+      const int mine = sh.tmp[t];
+      int rank = 0;
+      for (int k = 0; k < n; ++k) {
+        const int o = sh.tmp[k];
+        rank += (o > mine) || (o == mine && k < t);
+      }
+      order[rank] = t;
+    }
+    __syncthreads();
+  }
+  if (error) return;
+  for (int r = t; r < ts; r += kPlanThreads) seg_start[r] = cu_s[upper_index(cu_s, 0, ns, r)];
+  if (xrow)
+    for (int row = t; row < tp + ts; row += kPlanThreads) xrow_of(row, cu_p, cu_s, ng, ns, tp, ginfo, xrow);
 }
 
 }  // namespace pg
