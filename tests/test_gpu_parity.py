@@ -112,6 +112,22 @@ def test_small_full(case):
     _full_compare(prob)
 
 
+def test_more_groups_than_one_planner_pass():
+    """1100 groups, more than the planner's 1024 threads scan in one pass (and the multi-kernel planner,
+    since the tile lists no longer fit one block): tiny prefixes and responses, empty ones included,
+    every output and gradient against the oracle."""
+    rng = np.random.default_rng(11)
+    ng = 1100
+    prefix = rng.integers(0, 6, ng)
+    groups = rng.integers(0, 3, ng)
+    suffix = rng.integers(0, 5, int(groups.sum()))
+    prob = make_problem("single_group", seed=11, lengths=(prefix, groups, suffix), h_q=2, h_kv=1, head_dim=64,
+                        dtype="fp32", scale=0.125)
+    print(f"[parity] {ng} groups, {len(suffix)} members, total_prefix={prob.total_prefix} "
+          f"total_suffix={prob.total_suffix}", flush=True)
+    _full_compare(prob)
+
+
 def test_peaked_softmax_rescaling():
     """Q x 4: sharp rows exercise the running-max rescale of the online softmax."""
     prob = make_problem("single_group", seed=7, lengths=((700,), (3,), (300, 90, 211)), h_q=4, h_kv=1,

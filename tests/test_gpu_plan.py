@@ -19,7 +19,11 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
+_rng = np.random.default_rng(12)
+_G = _rng.integers(0, 3, 400)
 CASES = [
+    # 400 small groups: still one block's worth of tiles, several passes of nothing else
+    (tuple(_rng.integers(0, 70, 400)), tuple(_G), tuple(_rng.integers(0, 40, int(_G.sum()))), 2, 1, 64, "fp32"),
     ((257, 0, 40), (3, 2, 0), (129, 128, 1, 300, 0), 4, 2, 64, "bf16"),
     ((900,), (6,), (100, 300, 1, 250, 64, 129), 8, 2, 128, "bf16"),
     ((64,), (4,), (16, 31, 20, 32), 2, 2, 64, "fp32"),
