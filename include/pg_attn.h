@@ -49,6 +49,11 @@
  * only when the environment variable PG_DEBUG_VALIDATE=1 is set (which makes
  * the call synchronise), PG_EINVAL is returned. HIP failures return PG_EHIP.
  * pg_last_error() gives a message for the calling thread's last failure.
+ *
+ * Planning: each attention call first plans its tiles on the device, in one
+ * launch when every tile list fits one workgroup and in a short sequence of
+ * launches otherwise; both give the same plan. PG_PLAN_MULTI=1 in the
+ * environment forces the sequence (for testing).
  */
 #ifndef PG_ATTN_H
 #define PG_ATTN_H
