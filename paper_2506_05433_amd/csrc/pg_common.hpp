@@ -49,8 +49,24 @@ __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_lo
 // wave-uniform value held in a scalar register
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// The value of lane l and of lane l ^ 32, through gfx950's v_permlane32_swap (a VALU
+// exchange of the two half-waves; no LDS round trip, no wait on other LDS traffic).
+// With both operands equal to v, one result holds v of this lane's half and the other
+// v of the opposite half, on every lane.
+__device__ __forceinline__ void swap_halves(float v, float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  a = __uint_as_float(r[0]);
+  b = __uint_as_float(r[1]);
+}
 __device__ __forceinline__ float wave_swap32_max(float v) {
-  return fmaxf(v, __shfl_xor(v, 32));
+  float a, b;
+  swap_halves(v, a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float wave_swap32_sum(float v) {
+  float a, b;
+  swap_halves(v, a, b);
+  return a + b;
 }
 
 // ---------------------------------------------------------------- XCD-aware block order

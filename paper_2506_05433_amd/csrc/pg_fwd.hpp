@@ -290,7 +290,7 @@ __global__ void __launch_bounds__(kFwdThreads, 2) fwd_kernel(const FwdArgs a) {
   }
 
   if (!wave_active) return;
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = wave_swap32_sum(l_run);
   const float inv = 1.f / l_tot;
   if (qvalid) {
     T* O = (T*)(suffix ? a.o_suf : a.o_pre);

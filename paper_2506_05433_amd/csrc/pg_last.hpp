@@ -230,7 +230,7 @@ __global__ void __launch_bounds__(kLastThreads, 2) last_kernel(const LastArgs a)
   }
 
   if (!rvalid) return;
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = wave_swap32_sum(l_run);
   const size_t slotrow = ((size_t)((b * a.h_kv + kvh) * a.nch + chunk)) * kLastRows + r;
   float* po = a.part_o + slotrow * D;
 #pragma unroll
