@@ -187,6 +187,9 @@ int finish_plan(const pg::PlanHeader* hdr, hipStream_t st) {
   return PG_OK;
 }
 
+void launch_plan_tiles(const Common& c, const Layout& L, char* ws, const int32_t* cu_p, const int32_t* cu_s,
+                       const int32_t* gsz, hipStream_t st, bool bwd);
+
 // Runs the planner kernels. `bwd` also builds the key/value tile list.
 int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p, const int32_t* cu_s,
                 const int32_t* gsz, hipStream_t st, bool bwd, bool xl) {
@@ -195,15 +198,34 @@ int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p,
   auto* gi = (pg::GroupInfoEx*)(ws + L.ginfo);
   int* qoff = (int*)(ws + L.qoff);
   int* kvoff = (int*)(ws + L.kvoff);
+  auto* qt = (pg::TileDesc*)(ws + L.qtiles);
+  int* qo = (int*)(ws + L.qorder);
   if (L.max_q <= pg::kPlanThreads && (!bwd || L.max_kv <= pg::kPlanThreads) && !plan_multi()) {
-    // every tile list fits one block: the whole planner in one launch
+    // every tile list fits one block: groups, tiles and ranks in one launch
     hipLaunchKernelGGL(pg::plan_fused_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, cu_p, cu_s, gsz, c.ng, c.ns,
                        c.tp, c.ts, pg::kFwdBM, pg::kKvBN, L.kv_chunks, L.max_q, bwd ? L.max_kv : 0x7fffffffL, hdr, gi,
-                       qoff, kvoff, (pg::TileDesc*)(ws + L.qtiles), (int*)(ws + L.qorder),
-                       bwd ? (pg::TileDesc*)(ws + L.kvtiles) : nullptr, (int*)(ws + L.kvorder), (int*)(ws + L.seg),
-                       (bwd && xl) ? (int*)(ws + L.xrow) : nullptr);
-    return finish_plan(hdr, st);
+                       qoff, kvoff, qt, qo, bwd ? (pg::TileDesc*)(ws + L.kvtiles) : nullptr, (int*)(ws + L.kvorder));
+  } else {
+    launch_plan_tiles(c, L, ws, cu_p, cu_s, gsz, st, bwd);
   }
+  if (c.ts > 0) {
+    hipLaunchKernelGGL(pg::seg_start_kernel, dim3((unsigned)ceil_div_l(c.ts, 256)), dim3(256), 0, st, cu_s, c.ns,
+                       c.ts, hdr, (int*)(ws + L.seg));
+  }
+  if (bwd && xl && c.tp + c.ts > 0) {
+    hipLaunchKernelGGL(pg::xrow_kernel, dim3((unsigned)ceil_div_l((long)c.tp + c.ts, 256)), dim3(256), 0, st, cu_p,
+                       cu_s, c.ng, c.ns, c.tp, c.ts, hdr, gi, (int*)(ws + L.xrow));
+  }
+  return finish_plan(hdr, st);
+}
+
+// The multi-kernel planner: groups, then tiles and ranks of each list.
+void launch_plan_tiles(const Common& c, const Layout& L, char* ws, const int32_t* cu_p, const int32_t* cu_s,
+                       const int32_t* gsz, hipStream_t st, bool bwd) {
+  auto* hdr = (pg::PlanHeader*)(ws + L.hdr);
+  auto* gi = (pg::GroupInfoEx*)(ws + L.ginfo);
+  int* qoff = (int*)(ws + L.qoff);
+  int* kvoff = (int*)(ws + L.kvoff);
   hipLaunchKernelGGL(pg::plan_groups_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, cu_p, cu_s, gsz, c.ng, c.ns,
                      c.tp, c.ts, pg::kFwdBM, pg::kKvBN, L.kv_chunks, L.max_q, bwd ? L.max_kv : 0x7fffffffL, hdr, gi, qoff,
                      kvoff);
@@ -223,15 +245,6 @@ int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p,
                        L.kv_chunks, (int)L.max_kv, hdr, gi, kvoff, kt, 1);
     hipLaunchKernelGGL(pg::plan_rank_kernel, dim3(blocks), dim3(256), 0, st, hdr, kt, ko, 1);
   }
-  if (c.ts > 0) {
-    hipLaunchKernelGGL(pg::seg_start_kernel, dim3((unsigned)ceil_div_l(c.ts, 256)), dim3(256), 0, st, cu_s, c.ns,
-                       c.ts, hdr, (int*)(ws + L.seg));
-  }
-  if (bwd && xl && c.tp + c.ts > 0) {
-    hipLaunchKernelGGL(pg::xrow_kernel, dim3((unsigned)ceil_div_l((long)c.tp + c.ts, 256)), dim3(256), 0, st, cu_p,
-                       cu_s, c.ng, c.ns, c.tp, c.ts, hdr, gi, (int*)(ws + L.xrow));
-  }
-  return finish_plan(hdr, st);
 }
 
 template <typename T, int D>

@@ -258,19 +258,20 @@ __global__ void xrow_kernel(const int* __restrict__ cu_p, const int* __restrict_
   xrow_of(row, cu_p, cu_s, ng, ns, tp, ginfo, xrow);
 }
 
-// The whole planner in one block, for plans whose tile lists each fit in kPlanThreads
-// entries (the host checks the bounds): the steps above in order, separated by block
-// barriers instead of kernel boundaries, with the same results. Saves the launch and
-// memory latency of four to six dependent one-block kernels per call.
+// Groups, tile descriptors and longest-first ranks in one block, for plans whose tile
+// lists each fit in kPlanThreads entries (the host checks the bounds): the steps above in
+// order, separated by block barriers instead of kernel boundaries, with the same results.
+// Saves the launch and memory latency of two to four dependent one-block kernels per call.
+// The per-row tables (seg_start_kernel, xrow_kernel) stay separate wide launches: one
+// block would walk every row.
 __global__ void __launch_bounds__(kPlanThreads) plan_fused_kernel(
     const int* __restrict__ cu_p, const int* __restrict__ cu_s, const int* __restrict__ gsz, int ng, int ns, int tp,
     int ts, int bm, int bkv, int kv_chunks, long max_q, long max_kv, PlanHeader* hdr, GroupInfoEx* ginfo, int* qoff,
-    int* kvoff, TileDesc* qtiles, int* qorder, TileDesc* kvtiles, int* kvorder, int* seg_start, int* xrow) {
+    int* kvoff, TileDesc* qtiles, int* qorder, TileDesc* kvtiles, int* kvorder) {
   __shared__ PlanShared sh;
   plan_groups_body(cu_p, cu_s, gsz, ng, ns, tp, ts, bm, bkv, kv_chunks, max_q, max_kv, hdr, ginfo, qoff, kvoff, sh);
   __syncthreads();
   const int t = threadIdx.x;
-  const int error = hdr->error;
   const int nq = hdr->n_qtiles, nkv = kvtiles ? hdr->n_kvtiles : 0;  // both <= kPlanThreads (host bound)
   if (t < nq) plan_tile(t, cu_s, ng, bm, bkv, 1, ginfo, qoff, qtiles, 0);
   if (t < nkv) plan_tile(t, cu_s, ng, bm, bkv, kv_chunks, ginfo, kvoff, kvtiles, 1);
@@ -293,10 +294,6 @@ __global__ void __launch_bounds__(kPlanThreads) plan_fused_kernel(
     }
     __syncthreads();
   }
-  if (error) return;
-  for (int r = t; r < ts; r += kPlanThreads) seg_start[r] = cu_s[upper_index(cu_s, 0, ns, r)];
-  if (xrow)
-    for (int row = t; row < tp + ts; row += kPlanThreads) xrow_of(row, cu_p, cu_s, ng, ns, tp, ginfo, xrow);
 }
 
 }  // namespace pg
