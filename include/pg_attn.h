@@ -229,9 +229,9 @@ int pg_grouped_positions(int n_groups, int n_suffixes, int total_prefix, int tot
 typedef enum {
   PG_K_PLAN = 0,     /* the planner kernels of one call, as one interval      */
   PG_K_FWD = 1,      /* forward attention kernel                              */
-  PG_K_BWD_DOT = 2,  /* backward: rowsum(dO * O)                              */
+                     /* 2: unused (rowsum(dO * O) is formed inside the dQ kernel) */
   PG_K_DKDV = 3,     /* backward: dK, dV (key-stationary, G-way prefix sum)   */
-  PG_K_DQ = 4,       /* backward: dQ (query-stationary)                       */
+  PG_K_DQ = 4,       /* backward: dQ and rowsum(dO * O) (query-stationary)    */
   PG_K_ROPE = 5,     /* rotary embedding kernel of pg_rope                    */
   PG_K_LAST = 6      /* pg_attn_fwd_last: chunk kernel and merge, one interval */
 } pg_kernel;

@@ -256,11 +256,11 @@ void launch_fwd(const pg::FwdArgs& a, long max_q, hipStream_t st) {
 
 template <typename T, int D>
 void launch_bwd(const pg::BwdArgs& a, long max_q, long max_kv, hipStream_t st) {
-  const long rows = (long)a.total_prefix + a.total_suffix;
-  if (rows > 0) {
-    const long items = rows * a.h_q;
-    Timed tm(PG_K_BWD_DOT, st);
-    hipLaunchKernelGGL((pg::bwd_dot_kernel<T, D>), dim3((unsigned)ceil_div_l(items, 16)), dim3(256), 0, st, a);
+  // dQ first: it also writes Dsum, which the dK/dV kernel reads
+  if (max_q > 0) {
+    Timed tm(PG_K_DQ, st);
+    const long blocks = pg::xcd_grid_blocks(max_q, a.h_q, a.h_q / a.h_kv);
+    hipLaunchKernelGGL((pg::dq_kernel<T, D>), dim3((unsigned)blocks), dim3(pg::kDqThreads), 0, st, a);
   }
   if (max_kv > 0) {
     Timed tm(PG_K_DKDV, st);
@@ -270,11 +270,6 @@ void launch_bwd(const pg::BwdArgs& a, long max_q, long max_kv, hipStream_t st) {
       const long n = 2L * a.total_prefix * a.h_kv * D / 4;
       hipLaunchKernelGGL((pg::kv_reduce_kernel<T, D>), dim3((unsigned)ceil_div_l(n, 256)), dim3(256), 0, st, a);
     }
-  }
-  if (max_q > 0) {
-    Timed tm(PG_K_DQ, st);
-    const long blocks = pg::xcd_grid_blocks(max_q, a.h_q, a.h_q / a.h_kv);
-    hipLaunchKernelGGL((pg::dq_kernel<T, D>), dim3((unsigned)blocks), dim3(pg::kDqThreads), 0, st, a);
   }
 }
 

@@ -1,6 +1,8 @@
 // Backward kernels (vector-Jacobian product of the forward, Lemma 1 / Appendix A.1).
 //
-//   bwd_dot_kernel : Dsum[h][row] = <dO_row, O_row> (the softmax-Jacobian row term).
+//   dq_kernel      : query-stationary (the forward's tiling), recomputing P and dP. It runs
+//                    first and also forms Dsum[h][row] = <dO_row, O_row> (the softmax-Jacobian
+//                    row term) for its rows, which the dK/dV kernel then reads.
 //   dkdv_kernel    : key-stationary. A workgroup owns 128 keys of one key/value head
 //                    (32 per wave, kept in registers) and walks, in a fixed order, every
 //                    query row that sees them: for each query head sharing the kv head,
@@ -8,7 +10,6 @@
 //                    of the group. The prefix dK/dV of a group is therefore the G-way sum
 //                    of the members' contributions taken in member order inside one
 //                    workgroup: deterministic, no atomics.
-//   dq_kernel      : query-stationary (the forward's tiling), recomputing P and dP.
 //
 // Products per (query tile, key tile), all on 32x32 MFMA tiles:
 //   dkdv: S = Q K^T and dP = dO V^T with queries as rows (A = Q, dO from LDS, B = K, V
@@ -41,28 +42,6 @@ struct BwdArgs {
   int xl;
   const int* xrow;
 };
-
-// ------------------------------------------------------------------ Dsum = rowsum(dO * O)
-template <typename T, int D>
-__global__ void __launch_bounds__(256) bwd_dot_kernel(const BwdArgs a) {
-  // 16 lanes per (row, head); 16 rows-heads per 256-thread block
-  constexpr int EPL = D / 16;  // elements per lane
-  const int rows = a.total_prefix + a.total_suffix;
-  const long item = (long)blockIdx.x * 16 + (threadIdx.x >> 4);
-  const int sub = threadIdx.x & 15;
-  if (item >= (long)rows * a.h_q) return;
-  const int row = (int)(item / a.h_q), head = (int)(item % a.h_q);
-  const bool pre = row < a.total_prefix;
-  const int r = a.xl ? a.xrow[row] : (pre ? row : row - a.total_prefix);
-  const T* O = (const T*)(pre ? a.o_pre : a.o_suf) + ((size_t)r * a.h_q + head) * D + sub * EPL;
-  const T* G = (const T*)(pre ? a.do_pre : a.do_suf) + ((size_t)r * a.h_q + head) * D + sub * EPL;
-  float acc = 0.f;
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) acc += (float)O[e] * (float)G[e];
-#pragma unroll
-  for (int off = 8; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 16);
-  if (sub == 0) a.dsum[(size_t)head * rows + row] = acc;
-}
 
 // ------------------------------------------------------------------ dK, dV (key-stationary)
 // A workgroup owns 128 keys of one kv head, split into four groups of 32. Each key
@@ -440,7 +419,22 @@ __global__ void __launch_bounds__(kDqThreads, 2) dq_kernel(const BwdArgs a) {
   const float* L = suffix ? a.lse_suf : a.lse_pre;
   const int ld = a.xl ? rows_all : (suffix ? a.total_suffix : a.total_prefix);
   const float lse2 = L[(size_t)head * ld + qrow_c + xq] * kLog2e;
-  const float dsum = a.dsum[(size_t)head * rows_all + (suffix ? a.total_prefix : 0) + qrow_c];
+  // Dsum = <dO, O> of the lane's query: the lane holds half of the row (the dO fragments
+  // above), its partner lane (lane ^ 32) the other half. Stored for the dK/dV kernel.
+  float dsum;
+  {
+    const T* O = (const T*)(suffix ? a.o_suf : a.o_pre);
+    const size_t off = ((size_t)(qrow_c + xq) * a.h_q + head) * D + 8 * hh;
+    float part = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const Frag of = E::global_row(O + off + 16 * kk, qvalid);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) part = fmaf(E::frag_elem(of, e), E::frag_elem(gf[kk], e), part);
+    }
+    dsum = wave_swap32_sum(part);
+    if (qvalid && hh == 0) a.dsum[(size_t)head * rows_all + (suffix ? a.total_prefix : 0) + qrow] = dsum;
+  }
   const int seg_q = suffix ? a.seg_start[qrow_c] : 0;
   const int seg_w_lo = (suffix && wave_active) ? a.seg_start[wq0] : 0;
   const int seg_w_hi = (suffix && wave_active) ? a.seg_start[wq1] : 0;
