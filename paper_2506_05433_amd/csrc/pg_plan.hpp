@@ -143,7 +143,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_groups_kernel(
 }
 
 // Descriptor of tile i (< the number of tiles). `which` 0 = query tiles, 1 = kv tiles.
-__device__ inline void plan_tile(int i, const int* __restrict__ cu_s, int ng, int bm, int bkv, int kv_chunks,
+// Returns the tile's work (the ranking key).
+__device__ inline int plan_tile(int i, const int* __restrict__ cu_s, int ng, int bm, int bkv, int kv_chunks,
                                  const GroupInfoEx* __restrict__ ginfo, const int* __restrict__ off, TileDesc* tiles,
                                  int which) {
   const int g = upper_index(off, 0, ng, i);  // off[ng] == n > i, groups with no tile share offsets
@@ -186,6 +187,7 @@ __device__ inline void plan_tile(int i, const int* __restrict__ cu_s, int ng, in
     }
   }
   tiles[i] = d;
+  return d.work;
 }
 
 // One thread per (possible) tile: fills the descriptors.
@@ -272,16 +274,16 @@ __global__ void __launch_bounds__(kPlanThreads) plan_fused_kernel(
   plan_groups_body(cu_p, cu_s, gsz, ng, ns, tp, ts, bm, bkv, kv_chunks, max_q, max_kv, hdr, ginfo, qoff, kvoff, sh);
   __syncthreads();
   const int t = threadIdx.x;
-  const int nq = hdr->n_qtiles, nkv = kvtiles ? hdr->n_kvtiles : 0;  // both <= kPlanThreads (host bound)
-  if (t < nq) plan_tile(t, cu_s, ng, bm, bkv, 1, ginfo, qoff, qtiles, 0);
-  if (t < nkv) plan_tile(t, cu_s, ng, bm, bkv, kv_chunks, ginfo, kvoff, kvtiles, 1);
-  __syncthreads();
+  // the tile counts the header now holds, taken from shared memory (both <= kPlanThreads, a host bound)
+  const bool ok = !sh.err;
+  const int nq = ok ? sh.carry[1] : 0, nkv = (kvtiles && ok) ? sh.carry[2] : 0;
+  const int wq = t < nq ? plan_tile(t, cu_s, ng, bm, bkv, 1, ginfo, qoff, qtiles, 0) : -1;
+  const int wkv = t < nkv ? plan_tile(t, cu_s, ng, bm, bkv, kv_chunks, ginfo, kvoff, kvtiles, 1) : -1;
   // longest-first ranks, the rule of plan_rank_kernel: (work desc, index asc)
   for (int which = 0; which < 2; ++which) {
     const int n = which ? nkv : nq;
-    const TileDesc* tiles = which ? kvtiles : qtiles;
     int* order = which ? kvorder : qorder;
-    sh.tmp[t] = t < n ? tiles[t].work : -1;
+    sh.tmp[t] = which ? wkv : wq;
     __syncthreads();
     if (t < n) {
       const int mine = sh.tmp[t];
