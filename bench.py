@@ -204,7 +204,7 @@ def cpu_baseline(prob, useful_per_pair_head, budget_s):
         return time.perf_counter() - t0
 
     dt1 = run(1)
-    n_heads = max(1, min(prob.h_q, int(budget_s / max(dt1, 1e-3))))
+    n_heads = max(1, min(prob.h_q, round(budget_s / max(dt1, 1e-3))))
     dt = run(n_heads) if n_heads > 1 else dt1
     useful = useful_per_pair_head * pairs * n_heads
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
