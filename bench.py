@@ -320,7 +320,7 @@ def main():
     ap.add_argument("--workload", default="single_group")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-repeated", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--sweep", action="store_true",
                     help="run the paper's Fig. 2/3 grid (one JSON line per point) instead of the bench line")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
