@@ -1,22 +1,34 @@
 """Benchmark: grouped (shared-prefix) attention forward+backward on one MI355X.
 
-python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--no-repeated]
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--padded]
+                [--no-cpu-baseline] [--no-repeated] [--sweep]
 
 A step is one forward and one backward call over the whole workload (inputs
-resident in HBM). Prints ONE JSON line. ``value`` is useful TFLOP/s:
-4*d*H_q*pairs (forward) + 10*d*H_q*pairs (backward) per step, where pairs is
-the exact number of (query, key) pairs the grouped problem allows; masked
-work, ragged tiles and the repeated-prefix pairs the method avoids are not
-counted. The timed step is the forward and backward calls captured once as a
-HIP graph and replayed (the eager time of the same calls is reported too;
-per-kernel times come from HIP events in the eager pass). The same kernels
-are also timed on the repeated-prefix layout (every member with its own copy
-of the prefix) for the speedup.
+resident in HBM). The default workload is the largest one, ``packed_varlen``
+(8 groups, G=16, prefix lengths log-uniform in [1024, 32768], responses
+uniform in [64, 4096], 64/8 heads, d=128, bf16). Prints ONE JSON line.
+
+``value`` is useful TFLOP/s: 4*d*H_q*pairs (forward) + 10*d*H_q*pairs
+(backward) per step, where pairs is the exact number of (query, key) pairs the
+grouped problem allows; masked work, ragged tiles and the repeated-prefix
+pairs the method avoids are not counted.
+
+Timing protocol: W untimed warmup steps, then K timed steps. Before every
+timed step a 512 MiB buffer is overwritten (evicting the 256 MB Infinity
+Cache), and each step is bracketed by its own HIP events on the stream the
+library launches on; ``ms_per_step`` is the median. The timed step is the
+forward and backward calls captured once as a HIP graph and replayed; the
+same protocol on eager launches gives ``ms_per_step_eager`` and, through the
+library's own per-launch events, the per-kernel averages. The same kernels are
+timed on the repeated-prefix layout (every member with its own copy of the
+prefix; and with ``--padded`` also every member padded to the group's longest
+response, Eq. (1)) for the speedup.
 """
 import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -25,6 +37,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "grouped attn fwd+bwd TFLOP/s (useful) & % MFMA peak; speedup vs repeated-prefix"
 PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
+DEFAULT_WORKLOAD = "packed_varlen"
+FLUSH_BYTES = 512 << 20
 
 
 def pair_count(prefix_lens, group_sizes, suffix_lens):
@@ -51,12 +65,37 @@ def repeated_pair_count(prefix_lens, group_sizes, suffix_lens):
     return total
 
 
+def padded_pair_count(prefix_lens, group_sizes, suffix_lens):
+    """Pairs of the padded layout of Eq. (1): every member of a group padded to its longest response."""
+    total, m = 0, 0
+    for p, g in zip(prefix_lens, group_sizes):
+        g = int(g)
+        if g:
+            n = int(p) + int(max(suffix_lens[m:m + g]))
+            total += g * (n * (n + 1) // 2)
+        m += g
+    return total
+
+
 def progress(msg):
     """A progress line on stderr (the JSON result is the only stdout line)."""
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def time_steps(binding, torch, dev, bufs, steps, warmup):
+class Flusher:
+    """Overwrites a 512 MiB device buffer: run before each timed step so that no operand is served from the
+    256 MB Infinity Cache (or the L2s) left warm by the previous step."""
+
+    def __init__(self, torch):
+        self.buf = torch.empty(FLUSH_BYTES // 4, device="cuda", dtype=torch.float32)
+        self.k = 0
+
+    def __call__(self):
+        self.k += 1
+        self.buf.fill_(float(self.k & 7))
+
+
+def step_fn(binding, dev, bufs):
     def step():
         binding.fwd(dev["q_pre"], dev["k_pre"], dev["v_pre"], dev["q_suf"], dev["k_suf"], dev["v_suf"],
                     dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], dev["scale"], out=bufs["fwd"],
@@ -66,23 +105,49 @@ def time_steps(binding, torch, dev, bufs, steps, warmup):
                     o_pre, o_suf, lse_pre, lse_suf, dev["do_pre"], dev["do_suf"],
                     dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], dev["scale"], out=bufs["bwd"],
                     workspace=bufs["ws_b"])
+    return step
 
-    for _ in range(warmup):
+
+def timed_steps(torch, run, steps, flush, label):
+    """Per-step GPU times (ms) of ``run`` over ``steps`` steps, each after a cache flush and bracketed by its
+    own events on the current stream; the host waits for each step (progress lines every ~20 s)."""
+    times = []
+    t_last = time.monotonic()
+    for i in range(steps):
+        flush()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        run()
+        e1.record()
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+        if time.monotonic() - t_last > 20.0:
+            progress(f"{label}: step {i + 1}/{steps}, median so far {statistics.median(times):.3f} ms")
+            t_last = time.monotonic()
+    return times
+
+
+def time_layout(binding, torch, dev, bufs, steps, warmup, flush, label, eager=True):
+    """Graph-replay (and optionally eager) step times of one layout; per-kernel averages from the eager pass."""
+    step = step_fn(binding, dev, bufs)
+    out = {}
+    if eager:
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        binding.timing_start()
+        times = timed_steps(torch, step, steps, flush, label + " (eager)")
+        torch.cuda.synchronize()
+        binding.timing_stop()
+        out["eager_ms"] = times
+        kern = {}
+        for k in ("plan", "fwd", "dq", "dkdv", "kv_reduce"):
+            n, tot = binding.timing_get(k)
+            kern[k] = (tot / n) if n else None
+        out["kernels_ms"] = kern
+    else:
         step()
-    torch.cuda.synchronize()
-    binding.timing_start()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(steps):
-        step()
-    e1.record()
-    torch.cuda.synchronize()
-    binding.timing_stop()
-    ms = e0.elapsed_time(e1) / steps
-    kern = {}
-    for k in ("plan", "fwd", "dkdv", "dq"):
-        n, tot = binding.timing_get(k)
-        kern[k] = {"launches": n, "avg_ms": (tot / n) if n else None}
+        torch.cuda.synchronize()
     # the same step captured once as a HIP graph and replayed: no host launch cost per kernel
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -96,28 +161,89 @@ def time_steps(binding, torch, dev, bufs, steps, warmup):
     for _ in range(warmup):
         graph.replay()
     torch.cuda.synchronize()
-    e0.record()
-    for _ in range(steps):
-        graph.replay()
-    e1.record()
-    torch.cuda.synchronize()
-    ms_graph = e0.elapsed_time(e1) / steps
+    out["graph_ms"] = timed_steps(torch, graph.replay, steps, flush, label)
     del graph
-    return ms_graph, kern, ms
+    return out
 
 
-def alloc(binding, torch, dev, prob):
+def alloc(binding, torch, dev, prob_shape):
+    """Outputs and workspaces of one layout. ``prob_shape`` = (n_groups, n_suffixes, total_prefix,
+    total_suffix, h_q, h_kv, head_dim)."""
+    ng, ns, tp, ts, hq, hkv, d = prob_shape
     bufs = {
         "fwd": (torch.empty_like(dev["q_pre"]), torch.empty_like(dev["q_suf"]),
-                torch.empty((prob.h_q, prob.total_prefix), device="cuda", dtype=torch.float32),
-                torch.empty((prob.h_q, prob.total_suffix), device="cuda", dtype=torch.float32)),
+                torch.empty((hq, tp), device="cuda", dtype=torch.float32),
+                torch.empty((hq, ts), device="cuda", dtype=torch.float32)),
         "bwd": tuple(torch.empty_like(dev[k]) for k in ("q_pre", "k_pre", "v_pre", "q_suf", "k_suf", "v_suf")),
     }
-    args = (len(prob.prefix_lens), len(prob.suffix_lens), prob.total_prefix, prob.total_suffix, prob.h_q, prob.h_kv,
-            prob.head_dim)
-    bufs["ws_f"] = torch.empty(binding.workspace_bytes("fwd", *args), device="cuda", dtype=torch.uint8)
-    bufs["ws_b"] = torch.empty(binding.workspace_bytes("bwd", *args), device="cuda", dtype=torch.uint8)
+    bufs["ws_f"] = torch.empty(binding.workspace_bytes("fwd", *prob_shape), device="cuda", dtype=torch.uint8)
+    bufs["ws_b"] = torch.empty(binding.workspace_bytes("bwd", *prob_shape), device="cuda", dtype=torch.uint8)
     return bufs
+
+
+def shape_of(prob):
+    return (len(prob.prefix_lens), len(prob.suffix_lens), prob.total_prefix, prob.total_suffix, prob.h_q,
+            prob.h_kv, prob.head_dim)
+
+
+def baseline_layout(torch, dev, prob, padded):
+    """The repeated-prefix layout (Eq. (1) without padding), or with ``padded`` the padded one (every member's
+    response padded with zero rows to the group's longest), built on the device from the grouped tensors.
+
+    Every member becomes a group of size 1 holding its own copy of the group's prefix; ``do_pre`` goes whole
+    to a group's first copy and zero to the others, so the copies' summed prefix gradients equal the grouped
+    ones. Groups with no members keep their prefix as a group of size 0. Returns (device dict, shape)."""
+    import numpy as np
+    cu_p, cu_s = prob.cu_prefix, prob.cu_suffix
+    pre_idx, zero_do, prefix, groups, suffix, suf_src = [], [], [], [], [], []
+    m, row = 0, 0
+    for g, (p, gs) in enumerate(zip(prob.prefix_lens, prob.group_sizes)):
+        p, gs = int(p), int(gs)
+        rows = np.arange(cu_p[g], cu_p[g + 1])
+        width = int(max(prob.suffix_lens[m:m + gs])) if (gs and padded) else 0
+        for i in range(max(gs, 1)):
+            pre_idx.append(rows)
+            if i > 0:
+                zero_do.append(np.arange(row, row + p))
+            row += p
+            prefix.append(p)
+            groups.append(1 if gs else 0)
+            if gs:
+                s = int(prob.suffix_lens[m + i])
+                n = width if padded else s
+                src = np.full(n, -1, np.int64)
+                src[:s] = np.arange(cu_s[m + i], cu_s[m + i + 1])
+                suf_src.append(src)
+                suffix.append(n)
+        m += gs
+    cat = lambda xs: np.concatenate(xs) if xs else np.zeros(0, np.int64)  # noqa: E731
+    pre_idx, zero_do, suf_src = cat(pre_idx), cat(zero_do), cat(suf_src)
+    out = {}
+    where = dev["q_pre"].device
+    ipre = torch.from_numpy(pre_idx).to(where)
+    for name in ("q_pre", "k_pre", "v_pre", "do_pre"):
+        out[name] = dev[name].index_select(0, ipre)
+    if zero_do.size:
+        out["do_pre"].index_fill_(0, torch.from_numpy(zero_do).to(where), 0)
+    if padded:
+        # padding rows read row 0 and are then zeroed
+        isuf = torch.from_numpy(np.maximum(suf_src, 0)).to(where)
+        pad = torch.from_numpy(np.nonzero(suf_src < 0)[0]).to(where)
+        for name in ("q_suf", "k_suf", "v_suf", "do_suf"):
+            t = dev[name].index_select(0, isuf)
+            if pad.numel():
+                t.index_fill_(0, pad, 0)
+            out[name] = t
+    else:
+        for name in ("q_suf", "k_suf", "v_suf", "do_suf"):
+            out[name] = dev[name]
+    i32 = lambda a: torch.from_numpy(np.asarray(a, np.int32)).to(where)  # noqa: E731
+    out["cu_prefix"] = i32(np.concatenate([[0], np.cumsum(prefix)]))
+    out["cu_suffix"] = i32(np.concatenate([[0], np.cumsum(suffix)]))
+    out["group_sizes"] = i32(groups)
+    out["scale"] = prob.scale
+    shape = (len(prefix), len(suffix), int(sum(prefix)), int(sum(suffix)), prob.h_q, prob.h_kv, prob.head_dim)
+    return out, shape
 
 
 def time_last(binding, torch, dev, prob, steps, warmup):
@@ -179,39 +305,83 @@ def time_rope(binding, torch, dev, prob, steps, warmup):
     el = 2 if prob.dtype == "bf16" else 4
     nbytes = 2 * (prob.total_prefix + prob.total_suffix) * (prob.h_q + prob.h_kv) * prob.head_dim * el
     gbs = nbytes / (ms * 1e-3) / 1e9
+    del outs
     return {"kernel": "rope", "ms": round(ms, 4), "bytes": nbytes, "achieved_GBps": round(gbs, 1),
             "peak_GBps": 8000.0, "frac": round(gbs / 8000.0, 4), "bound": "hbm"}
 
 
-def cpu_baseline(prob, useful_per_pair_head, budget_s):
-    """The oracle (fp64 numpy, as it stands) on a bounded sample of the workload.
+def sub_problem(prob, g, h):
+    """Group g and query head h of ``prob`` as a problem of its own (one query head and its key/value head),
+    decoded to float64: the unit the CPU oracle is timed on."""
+    import numpy as np
+    cu_p, cu_s = prob.cu_prefix, prob.cu_suffix
+    m0 = int(prob.group_sizes[:g].sum())
+    m1 = m0 + int(prob.group_sizes[g])
+    p0, p1, s0, s1 = int(cu_p[g]), int(cu_p[g + 1]), int(cu_s[m0]), int(cu_s[m1])
+    kv = h // (prob.h_q // prob.h_kv)
+    t = {}
+    for name, a in prob.tensors.items():
+        rows = slice(p0, p1) if name.endswith("_pre") else slice(s0, s1)
+        hs = slice(kv, kv + 1) if name[0] in "kv" else slice(h, h + 1)
+        a = np.ascontiguousarray(a[rows, hs])
+        if a.dtype == np.uint16:
+            a = (a.astype(np.uint32) << 16).view(np.float32)
+        t[name] = a.astype(np.float64)
+    lengths = (np.array([p1 - p0]), np.array([m1 - m0]), np.asarray(prob.suffix_lens[m0:m1]))
+    return lengths, t
 
-    The sample is all rows and members of the first k query heads, fwd+bwd; one head is
-    timed first and k is chosen so the measured run takes about ``budget_s`` seconds.
-    """
+
+def cpu_baseline(prob, budget_s):
+    """The oracle (fp64 numpy, as it stands) on a bounded sample of the workload: whole (group, query head)
+    units, fwd+bwd, timed one call at a time.
+
+    The smallest group's first head is timed first; that rate picks the group by work rank (the median
+    group, or a smaller one if one of its heads would take more than ~40 s), whose heads then run until the
+    budget is spent. ``value`` = useful flops of the units run (14*d per grouped pair and head, as for the
+    GPU) / their total time."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
     from oracle import grouped_oracle
-    t = {k: prob.as_float(k, np.float64) for k in prob.tensors}
-    pairs_rep = repeated_pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
-    pairs = pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
+    ng = len(prob.prefix_lens)
+    cs = np.concatenate([[0], np.cumsum(prob.group_sizes)])
+    per_group = []
+    for g in range(ng):
+        lens = ([prob.prefix_lens[g]], [prob.group_sizes[g]], prob.suffix_lens[cs[g]:cs[g + 1]])
+        per_group.append((repeated_pair_count(*lens), pair_count(*lens)))
+    order = [g for g in sorted(range(ng), key=lambda g: per_group[g][0]) if per_group[g][0] > 0]
+    useful_per_pair = 14.0 * prob.head_dim
+    units, total_s, total_flops = [], 0.0, 0.0
 
-    def run(n):
+    def run(g, h):
+        nonlocal total_s, total_flops
+        lengths, t = sub_problem(prob, g, h)
         t0 = time.perf_counter()
-        grouped_oracle(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, grads=True,
-                       heads=list(range(n)), check_members=False)
-        return time.perf_counter() - t0
+        grouped_oracle(*lengths, t, prob.scale, grads=True, check_members=False)
+        dt = time.perf_counter() - t0
+        total_s += dt
+        total_flops += useful_per_pair * per_group[g][1]
+        units.append((g, h))
+        progress(f"cpu oracle: group {g} head {h}: {dt:.1f} s")
+        return dt
 
-    dt1 = run(1)
-    n_heads = max(1, min(prob.h_q, round(budget_s / max(dt1, 1e-3))))
-    dt = run(n_heads) if n_heads > 1 else dt1
-    useful = useful_per_pair_head * pairs * n_heads
+    if not order:
+        return None
+    g0 = order[0]
+    rate = per_group[g0][0] / max(run(g0, 0), 1e-6)  # repeated pairs per second
+    cand = [g for g in order if per_group[g][0] / rate <= min(40.0, budget_s)]
+    g1 = cand[min(len(cand) - 1, len(order) // 2)] if cand else g0
+    h = 0 if g1 != g0 else 1
+    while h < prob.h_q and total_s + per_group[g1][0] / rate <= budget_s:
+        run(g1, h)
+        h += 1
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    return {"value": useful / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{n_heads} of {prob.h_q} query heads, all rows and members, fp64 numpy, repeated-prefix "
-                      f"({pairs_rep} repeated pairs per head), fwd+bwd; {dt:.1f} s",
-            "seconds": round(dt, 2), "host_cpus": len(os.sched_getaffinity(0))}
+    desc = ", ".join(f"g{g}h{h}" for g, h in units)
+    return {"value": total_flops / total_s / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{len(units)} (group, query head) units [{desc}] of {ng} groups x {prob.h_q} heads "
+                      f"(groups P={[int(prob.prefix_lens[g]) for g in sorted(set(u[0] for u in units))]}), "
+                      f"all rows and members of each, fp64 numpy, repeated-prefix, fwd+bwd; {total_s:.1f} s",
+            "seconds": round(total_s, 2), "host_cpus": len(os.sched_getaffinity(0))}
 
 
 ATTN_SOURCES = ("pg_attn.hip", "pg_bwd.hpp", "pg_common.hpp", "pg_fwd.hpp", "pg_plan.hpp")
@@ -246,6 +416,19 @@ def recorded_traffic(kernel, workload):
     return f + w
 
 
+def recorded_trace_us(kernel, workload):
+    """Average duration (us) of ``kernel`` from the rocprofv3 kernel-trace summary
+    profiles/trace_<workload>.json, if taken on this source, else None."""
+    path = os.path.join(ROOT, "profiles", f"trace_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        t = json.load(fh)
+    if t.get("source_sha") != kernel_source_sha():
+        return None
+    return t.get("avg_us", {}).get(kernel)
+
+
 def calibrate_copy(n_bytes):
     """A plain device-to-device copy of n_bytes (reference reading for the HBM byte counters)."""
     import torch
@@ -258,55 +441,77 @@ def calibrate_copy(n_bytes):
     print(json.dumps({"copy_bytes": n_bytes, "launches": 3}))
 
 
-def tensor_bytes(prob, grads=True):
-    """Device bytes of the layer's tensors for one layout (inputs, outputs, LSE and, with grads, dO and dQ/dK/dV)."""
-    el = 2 if prob.dtype == "bf16" else 4
-    rows = prob.total_prefix + prob.total_suffix
-    per_row = (2 * prob.h_q + 2 * prob.h_kv) * prob.head_dim * el + prob.h_q * 4  # q, o, k, v, lse
-    if grads:
-        per_row += (2 * prob.h_q + 2 * prob.h_kv) * prob.head_dim * el  # do, dq, dk, dv
-    return rows * per_row
+def measured_peak_bytes(torch, build):
+    """Peak device bytes allocated while ``build()`` allocates a layout and runs one fwd+bwd step on it,
+    above what was allocated before (torch's allocator statistics; the library allocates nothing)."""
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    base = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
+    keep = build()
+    torch.cuda.synchronize()
+    peak = torch.cuda.max_memory_allocated() - base
+    return peak, keep
 
 
 def sweep(args):
     """Fig. 2/3 grid of the paper: prefix 4096/8192/16384, G in {2,4,8,16}, prefix/response ratio r.
 
-    Every member has the same response length P / r (the setting of Appendix A.2). For each point the
-    grouped and the repeated layouts run the same kernels; the line reports both times, the speedup,
-    Eq. (17)'s attention-cost ratio, the useful TFLOP/s and the tensor + workspace bytes of both layouts.
+    Member i's response length is drawn uniform in [S/2, 3S/2] with S = P / r (the ratio is prefix over mean
+    response), so the padded layout of Eq. (1) differs from the unpadded repeated one. For each point the
+    grouped, repeated and padded layouts run the same kernels; the line reports the three times, the
+    speedups, Eq. (17)'s attention-cost ratio at the mean lengths, the useful TFLOP/s, and each layout's
+    measured peak device memory for one fwd+bwd step (inputs, outputs, gradients and workspaces).
     """
     import torch
 
     from paper_2506_05433_amd import binding
-    from paper_2506_05433_amd.inputs import Workload, make_problem, repeated_layout
+    from paper_2506_05433_amd.inputs import Workload, make_problem
+    flush = Flusher(torch)
     rows = []
     for P in (4096, 8192, 16384):
         for G in (2, 4, 8, 16):
             for r in (1, 4, 16):
                 S = P // r
-                wl = Workload(f"sweep_P{P}_G{G}_r{r}", 1, G, ("fixed", P), ("uniform", S, S), 32, 8, 128, "bf16",
-                              1.0 / 128 ** 0.5)
+                wl = Workload(f"sweep_P{P}_G{G}_r{r}", 1, G, ("fixed", P), ("uniform", S // 2, S + S // 2), 32, 8,
+                              128, "bf16", 1.0 / 128 ** 0.5)
                 prob = make_problem(wl, seed=0)
                 pairs = pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
                 flops = 14.0 * 128 * 32 * pairs
-                out = {"P": P, "G": G, "r": r, "S": S}
-                for name, pr in (("grouped", prob), ("repeated", repeated_layout(prob))):
-                    # names the case before any GPU work on it, on stdout
-                    print(f"[sweep] P={P} G={G} r={r} {name}: groups={len(pr.prefix_lens)} "
-                          f"total_prefix={pr.total_prefix} total_suffix={pr.total_suffix}", flush=True)
-                    dev = binding.to_device(pr, "cuda")
-                    bufs = alloc(binding, torch, dev, pr)
-                    ms, _, _ = time_steps(binding, torch, dev, bufs, args.steps, args.warmup)
-                    ws = sum(b.numel() for b in (bufs["ws_f"], bufs["ws_b"]))
-                    out[name + "_ms"] = round(ms, 4)
-                    out[name + "_MB"] = round((tensor_bytes(pr) + ws) / 1e6, 1)
+                out = {"P": P, "G": G, "r": r, "S_mean": S, "S": [int(x) for x in prob.suffix_lens]}
+                for name in ("grouped", "repeated", "padded"):
+                    # names the case before any GPU work on it
+                    print(f"[sweep] P={P} G={G} r={r} {name}", flush=True)
+
+                    def build():
+                        dev = binding.to_device(prob, "cuda")
+                        shape = shape_of(prob)
+                        if name != "grouped":
+                            bdev, shape = baseline_layout(torch, dev, prob, padded=name == "padded")
+                            del dev
+                            dev = bdev
+                        bufs = alloc(binding, torch, dev, shape)
+                        step_fn(binding, dev, bufs)()
+                        return dev, bufs
+
+                    peak, (dev, bufs) = measured_peak_bytes(torch, build)
+                    res = time_layout(binding, torch, dev, bufs, args.steps, args.warmup, flush, name, eager=False)
+                    out[name + "_ms"] = round(statistics.median(res["graph_ms"]), 4)
+                    out[name + "_peak_MB"] = round(peak / 1e6, 1)
                     del dev, bufs
                     torch.cuda.empty_cache()
-                eq17 = (P * P + G * S * (2 * P + S)) / (G * (P + S) ** 2)
-                out.update({"speedup": round(out["repeated_ms"] / out["grouped_ms"], 3),
+                Lr = S
+                eq17 = (P * P + G * Lr * (2 * P + Lr)) / (G * (P + Lr) ** 2)
+                out.update({"speedup_vs_repeated": round(out["repeated_ms"] / out["grouped_ms"], 3),
+                            "speedup_vs_padded": round(out["padded_ms"] / out["grouped_ms"], 3),
                             "eq17_cost_ratio": round(eq17, 4), "eq17_speedup": round(1 / eq17, 3),
+                            "pair_ratio_repeated": round(repeated_pair_count(prob.prefix_lens, prob.group_sizes,
+                                                                             prob.suffix_lens) / pairs, 3),
+                            "pair_ratio_padded": round(padded_pair_count(prob.prefix_lens, prob.group_sizes,
+                                                                         prob.suffix_lens) / pairs, 3),
                             "useful_tflops": round(flops / (out["grouped_ms"] * 1e-3) / 1e12, 1),
-                            "memory_ratio": round(out["grouped_MB"] / out["repeated_MB"], 3)})
+                            "memory_ratio_repeated": round(out["grouped_peak_MB"] / out["repeated_peak_MB"], 3),
+                            "memory_ratio_padded": round(out["grouped_peak_MB"] / out["padded_peak_MB"], 3)})
                 print(json.dumps(out), flush=True)
                 rows.append(out)
     return rows
@@ -315,11 +520,13 @@ def sweep(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="single_group")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-repeated", action="store_true")
+    ap.add_argument("--padded", action="store_true", help="also time the padded layout of Eq. (1)")
+    ap.add_argument("--no-extras", action="store_true", help="skip the rotary-embedding and final-token timings")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--sweep", action="store_true",
                     help="run the paper's Fig. 2/3 grid (one JSON line per point) instead of the bench line")
@@ -341,68 +548,89 @@ def main():
     import torch
 
     from paper_2506_05433_amd import binding
-    from paper_2506_05433_amd.inputs import WORKLOADS, make_problem, repeated_layout
+    from paper_2506_05433_amd.inputs import WORKLOADS, make_problem
 
     wl = WORKLOADS[args.workload]
     progress(f"{wl.name}: generating inputs")
+    t0 = time.monotonic()
     prob = make_problem(wl, seed=0)
     d, hq = prob.head_dim, prob.h_q
     pairs = pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
     rep_pairs = repeated_pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens)
     fwd_flops = 4.0 * d * hq * pairs
     bwd_flops = 10.0 * d * hq * pairs
+    progress(f"{wl.name}: pairs={pairs} tokens={prob.total_prefix + prob.total_suffix} "
+             f"(inputs drawn in {time.monotonic() - t0:.0f} s)")
+    flush = Flusher(torch)
     dev = binding.to_device(prob, "cuda")
-    bufs = alloc(binding, torch, dev, prob)
-    print(f"[bench] {wl.name}: pairs={pairs} tokens={prob.total_prefix + prob.total_suffix}", file=sys.stderr,
-          flush=True)
-    ms, kern, ms_eager = time_steps(binding, torch, dev, bufs, args.steps, args.warmup)
-    progress(f"grouped layout: {ms:.3f} ms/step")
+    bufs = alloc(binding, torch, dev, shape_of(prob))
+    res = time_layout(binding, torch, dev, bufs, args.steps, args.warmup, flush, "grouped")
+    ms = statistics.median(res["graph_ms"])
+    ms_eager = statistics.median(res["eager_ms"])
+    kern = res["kernels_ms"]
+    progress(f"grouped layout: {ms:.3f} ms/step (median of {args.steps})")
     value = (fwd_flops + bwd_flops) / (ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[prob.dtype]
     algo = {"fwd": fwd_flops, "dkdv": 8.0 * d * hq * pairs, "dq": 6.0 * d * hq * pairs}
-    dom = max(("fwd", "dkdv", "dq"), key=lambda k: (kern[k]["avg_ms"] or 0.0))
-    achieved = algo[dom] / (kern[dom]["avg_ms"] * 1e-3) / 1e12
-    fwd_ms = kern["fwd"]["avg_ms"]
-    bwd_ms = sum(kern[k]["avg_ms"] or 0.0 for k in ("dkdv", "dq"))
+    dom = max(("fwd", "dkdv", "dq"), key=lambda k: (kern[k] or 0.0))
+    achieved = algo[dom] / (kern[dom] * 1e-3) / 1e12
+    fwd_ms = kern["fwd"]
+    bwd_ms = sum(kern[k] or 0.0 for k in ("dkdv", "dq", "kv_reduce"))
+    roof = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": recorded_traffic(dom, wl.name),
+            "algorithmic_flops": algo[dom], "avg_ms_events": round(kern[dom], 4),
+            "source_sha": kernel_source_sha()}
+    tr = recorded_trace_us(dom, wl.name)
+    if tr:
+        roof["avg_ms_trace"] = round(tr / 1e3, 4)
+        roof["frac_trace"] = round(algo[dom] / (tr * 1e-6) / 1e12 / peak, 4)
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": prob.dtype, "data": "synthetic (seeded normal inputs, lengths drawn per workload)",
+        "vs_baseline": None, "dtype": prob.dtype,
+        "data": "synthetic (seeded normal inputs, lengths drawn per workload)",
         "config": {"workload": wl.name, "desc": wl.note, "n_groups": int(len(prob.prefix_lens)),
                    "total_prefix": prob.total_prefix, "total_suffix": prob.total_suffix, "h_q": hq,
                    "h_kv": prob.h_kv, "head_dim": d, "pairs": pairs, "parallelism": "single GPU"},
-        "ms_per_step_eager": round(ms_eager, 4), "step": "one HIP-graph replay of fwd+bwd (eager launches: "
-                                                         "ms_per_step_eager)",
+        "timing": f"median of {args.steps} HIP-graph replays of fwd+bwd, each after a 512 MiB cache-evicting "
+                  f"write; eager launches: ms_per_step_eager",
+        "ms_per_step_mean": round(statistics.fmean(res["graph_ms"]), 4),
+        "ms_per_step_eager": round(ms_eager, 4),
         "pct_of_peak": round(100.0 * value / peak, 2),
         "fwd_tflops": round(fwd_flops / (fwd_ms * 1e-3) / 1e12, 2) if fwd_ms else None,
         "bwd_tflops": round(bwd_flops / (bwd_ms * 1e-3) / 1e12, 2) if bwd_ms else None,
-        "kernels_ms": {k: (round(v["avg_ms"], 4) if v["avg_ms"] else None) for k, v in kern.items()},
-        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
-                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-                     "traffic": recorded_traffic(dom, wl.name), "source_sha": kernel_source_sha()},
+        "kernels_ms": {k: (round(v, 4) if v else None) for k, v in kern.items()},
+        "roofline": roof,
     }
-    out["rope"] = time_rope(binding, torch, dev, prob, args.steps, args.warmup)
-    out["last"] = time_last(binding, torch, dev, prob, args.steps, args.warmup)
+    if not args.no_extras:
+        out["rope"] = time_rope(binding, torch, dev, prob, args.steps, args.warmup)
+        out["last"] = time_last(binding, torch, dev, prob, args.steps, args.warmup)
     if not args.no_repeated:
-        progress("building the repeated-prefix layout")
-        rep = repeated_layout(prob)
-        del dev, bufs
-        torch.cuda.empty_cache()
-        rdev = binding.to_device(rep, "cuda")
-        rbufs = alloc(binding, torch, rdev, rep)
-        rms, _, _ = time_steps(binding, torch, rdev, rbufs, args.steps, args.warmup)
-        progress(f"repeated layout: {rms:.3f} ms/step")
-        G = prob.group_sizes
-        P = prob.prefix_lens
-        sum_s = prob.suffix_lens.sum()
-        target = 0.8 * float((G * P).sum() + sum_s) / float(P.sum() + sum_s)
-        out.update({"repeated_ms_per_step": round(rms, 4), "speedup_vs_repeated": round(rms / ms, 3),
-                    "speedup_target": round(target, 3), "speedup_ceiling_pairs": round(rep_pairs / pairs, 3)})
-        del rdev, rbufs
+        out["speedup_ceiling_pairs"] = round(rep_pairs / pairs, 3)
+        G, P, sum_s = prob.group_sizes, prob.prefix_lens, prob.suffix_lens.sum()
+        out["speedup_target"] = round(0.8 * float((G * P).sum() + sum_s) / float(P.sum() + sum_s), 3)
+        del bufs
+        layouts = ["repeated"] + (["padded"] if args.padded else [])
+        for name in layouts:
+            progress(f"building the {name} layout on the device")
+            bdev, shape = baseline_layout(torch, dev, prob, padded=name == "padded")
+            bbufs = alloc(binding, torch, bdev, shape)
+            r = time_layout(binding, torch, bdev, bbufs, args.steps, args.warmup, flush, name, eager=False)
+            rms = statistics.median(r["graph_ms"])
+            progress(f"{name} layout: {rms:.3f} ms/step")
+            out[f"{name}_ms_per_step"] = round(rms, 4)
+            out[f"speedup_vs_{name}"] = round(rms / ms, 3)
+            del bdev, bbufs
+            torch.cuda.empty_cache()
+        if args.padded:
+            out["speedup_ceiling_pairs_padded"] = round(
+                padded_pair_count(prob.prefix_lens, prob.group_sizes, prob.suffix_lens) / pairs, 3)
+    del dev
+    torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         progress("timing the CPU oracle on a sample")
-        out["cpu_baseline"] = cpu_baseline(prob, 14.0 * d, args.cpu_budget)
-    print(json.dumps(out))
+        out["cpu_baseline"] = cpu_baseline(prob, args.cpu_budget)
+    print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":

@@ -233,7 +233,8 @@ typedef enum {
   PG_K_DKDV = 3,     /* backward: dK, dV (key-stationary, G-way prefix sum)   */
   PG_K_DQ = 4,       /* backward: dQ and rowsum(dO * O) (query-stationary)    */
   PG_K_ROPE = 5,     /* rotary embedding kernel of pg_rope                    */
-  PG_K_LAST = 6      /* pg_attn_fwd_last: chunk kernel and merge, one interval */
+  PG_K_LAST = 6,     /* pg_attn_fwd_last: chunk kernel and merge, one interval */
+  PG_K_KV_REDUCE = 7 /* backward: fixed-order sum of the prefix dK/dV partials  */
 } pg_kernel;
 
 int pg_timing_start(void);

@@ -62,7 +62,7 @@ def lib():
     return _lib
 
 
-KERNELS = {"plan": 0, "fwd": 1, "dkdv": 3, "dq": 4, "rope": 5, "last": 6}
+KERNELS = {"plan": 0, "fwd": 1, "dkdv": 3, "dq": 4, "rope": 5, "last": 6, "kv_reduce": 7}
 ROPE_INVERSE, ROPE_INTERLEAVED = 1, 2
 
 

@@ -263,10 +263,13 @@ void launch_bwd(const pg::BwdArgs& a, long max_q, long max_kv, hipStream_t st) {
     hipLaunchKernelGGL((pg::dq_kernel<T, D>), dim3((unsigned)blocks), dim3(pg::kDqThreads), 0, st, a);
   }
   if (max_kv > 0) {
-    Timed tm(PG_K_DKDV, st);
-    const long blocks = pg::xcd_grid_blocks(max_kv, a.h_kv, 1);
-    hipLaunchKernelGGL((pg::dkdv_kernel<T, D>), dim3((unsigned)blocks), dim3(pg::kKvThreads), 0, st, a);
+    {
+      Timed tm(PG_K_DKDV, st);
+      const long blocks = pg::xcd_grid_blocks(max_kv, a.h_kv, 1);
+      hipLaunchKernelGGL((pg::dkdv_kernel<T, D>), dim3((unsigned)blocks), dim3(pg::kKvThreads), 0, st, a);
+    }
     if (a.kv_chunks > 1 && a.total_prefix > 0) {
+      Timed tm(PG_K_KV_REDUCE, st);
       const long n = 2L * a.total_prefix * a.h_kv * D / 4;
       hipLaunchKernelGGL((pg::kv_reduce_kernel<T, D>), dim3((unsigned)ceil_div_l(n, 256)), dim3(256), 0, st, a);
     }

@@ -73,3 +73,70 @@ def test_traffic_is_reported_only_for_the_profiled_sources(tmp_path, monkeypatch
         fh.write("// edit\n")
     assert bench.kernel_source_sha() != digest
     assert bench.recorded_traffic("dkdv", "w") is None
+
+
+def _cpu_dev(prob):
+    import torch
+    out = {}
+    for name, a in prob.tensors.items():
+        t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16) if a.dtype == np.uint16 \
+            else torch.from_numpy(np.ascontiguousarray(a))
+        out[name] = t
+    out["scale"] = prob.scale
+    return out
+
+
+def test_device_repeated_layout_matches_host_construction():
+    """bench's repeated layout (built with index_select) equals inputs.repeated_layout, empty groups included."""
+    from paper_2506_05433_amd.inputs import make_problem, repeated_layout
+    import torch
+    prob = make_problem("single_group", seed=2, lengths=((5, 0, 7, 3), (2, 1, 0, 3), (4, 0, 6, 1, 2, 3)), h_q=4,
+                        h_kv=2, head_dim=64)
+    got, shape = bench.baseline_layout(torch, _cpu_dev(prob), prob, padded=False)
+    ref = repeated_layout(prob)
+    assert shape == bench.shape_of(ref)
+    assert got["cu_prefix"].tolist() == ref.cu_prefix.tolist()
+    assert got["cu_suffix"].tolist() == ref.cu_suffix.tolist()
+    assert got["group_sizes"].tolist() == ref.group_sizes.tolist()
+    for name, a in ref.tensors.items():
+        assert np.array_equal(got[name].view(torch.int16).numpy().view(np.uint16), a), name
+
+
+def test_device_padded_layout():
+    """Padded layout of Eq. (1): member i of a group keeps its rows and gets zero rows up to the group's
+    longest response; pair count = sum over members of (P + max S)(P + max S + 1) / 2."""
+    from paper_2506_05433_amd.inputs import make_problem
+    import torch
+    lengths = ((5, 3), (3, 2), (4, 1, 6, 2, 2))
+    prob = make_problem("single_group", seed=2, lengths=lengths, h_q=2, h_kv=1, head_dim=64, dtype="fp32")
+    got, shape = bench.baseline_layout(torch, _cpu_dev(prob), prob, padded=True)
+    assert got["cu_suffix"].tolist() == [0, 6, 12, 18, 20, 22]
+    assert got["cu_prefix"].tolist() == [0, 5, 10, 15, 18, 21]
+    q = got["q_suf"].numpy()
+    src = prob.tensors["q_suf"]
+    assert np.array_equal(q[0:4], src[0:4]) and not q[4:6].any()
+    assert np.array_equal(q[6:7], src[4:5]) and not q[7:12].any()
+    assert np.array_equal(q[12:18], src[5:11])
+    assert np.array_equal(q[20:22], src[13:15])
+    # do_pre only on the first copy of each group's prefix
+    dp = got["do_pre"].numpy()
+    assert np.array_equal(dp[0:5], prob.tensors["do_pre"][0:5]) and not dp[5:15].any()
+    assert bench.padded_pair_count(*lengths) == 3 * (11 * 12 // 2) + 2 * (5 * 6 // 2)
+    assert bench.padded_pair_count(*lengths) == bench.repeated_pair_count(
+        got["cu_prefix"].diff().numpy(), np.ones(5, int), got["cu_suffix"].diff().numpy())
+
+
+def test_cpu_baseline_units_are_the_oracle_on_one_group_and_head():
+    """The CPU leg's (group, head) sub-problem gives the full oracle's rows of that group and head."""
+    from oracle import grouped_oracle
+    from paper_2506_05433_amd.inputs import make_problem
+    prob = make_problem("single_group", seed=3, lengths=((6, 4), (2, 3), (3, 1, 5, 2, 4)), h_q=4, h_kv=2,
+                        head_dim=64)
+    t = {k: prob.as_float(k) for k in prob.tensors}
+    full = grouped_oracle(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale)
+    lengths, sub = bench.sub_problem(prob, 1, 3)
+    r = grouped_oracle(*lengths, sub, prob.scale)
+    assert np.array_equal(r["o_pre"][:, 0], full["o_pre"][6:10, 3])
+    assert np.array_equal(r["dq_suf"][:, 0], full["dq_suf"][4:15, 3])
+    res = bench.cpu_baseline(prob, 1.0)
+    assert res["kind"] == "oracle" and res["value"] > 0 and res["cores"] >= 1
