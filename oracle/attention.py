@@ -187,16 +187,22 @@ def _group_of_prefix_row(cu_p, row):
 
 
 def query_rows(prefix_lens, group_sizes, suffix_lens, t, scale, side, rows, heads, grads=True,
-               dtype=np.float64):
-    """Outputs of selected query rows, each computed on its own (Eq. (3) for one row).
+               dtype=np.float64, batch=256):
+    """Outputs of selected query rows, each row from its own keys (Eq. (3) for one row).
 
     ``side`` is "pre" or "suf"; ``rows`` are packed row indices on that side;
     ``heads`` are query heads. A prefix row of group g at offset j sees prefix
     keys 0..j of its group; a suffix row at offset j of member i sees its
     group's whole prefix and response keys 0..j of member i ([P; R_i],
-    Eq. (1)). For a prefix row the gradient is summed over the G copies, each
-    with do_pre / G (Lemma 1); since every copy sees the same keys this is the
-    single-row gradient with do_pre computed G times and summed.
+    Eq. (1)). For a prefix row the gradient is the sum over the G copies of
+    the row, each carrying do_pre / G (Lemma 1); every copy sees the same keys
+    and gives the same value, so the sum is G times one copy's.
+
+    The requested rows are evaluated together where they read the same keys:
+    the rows of one prefix (or one member's response) and the query heads of
+    one key/value head form the rows of one matrix product over that
+    sequence's keys, each row masked to the keys it sees; the softmax of every
+    row is exact over its keys. ``batch`` bounds the rows of one product.
 
     Returns dict o [len(rows), len(heads), d], lse [len(heads), len(rows)]
     and, with ``grads``, dq like o.
@@ -205,50 +211,68 @@ def query_rows(prefix_lens, group_sizes, suffix_lens, t, scale, side, rows, head
     cu_s = np.concatenate([[0], np.cumsum(suffix_lens)]).astype(np.int64)
     h_q, d = t["q_pre"].shape[1], t["q_pre"].shape[2]
     h_kv = t["k_pre"].shape[1]
+    rows = [int(r) for r in rows]
+    heads = [int(h) for h in heads]
     nr, nh = len(rows), len(heads)
     o = np.zeros((nr, nh, d), dtype)
     lse = np.zeros((nh, nr), dtype)
     dq = np.zeros((nr, nh, d), dtype)
-    f = lambda name: t[name]  # noqa: E731
+    f = lambda name, idx: np.asarray(t[name][idx], dtype)  # noqa: E731
+    # owner of a row's key set: ("pre", group) or ("suf", member)
+    owners = {}
     for a, row in enumerate(rows):
-        row = int(row)
-        if side == "pre":
-            g = _group_of_prefix_row(cu_p, row)
+        key = ("pre", _group_of_prefix_row(cu_p, row)) if side == "pre" else ("suf", _member_of(cu_s, row))
+        owners.setdefault(key, []).append(a)
+    for (kind, idx), members in owners.items():
+        last = max(rows[a] for a in members)
+        if kind == "pre":
+            g = idx
             p0 = int(cu_p[g])
-            keys_k = [f("k_pre")[p0:row + 1]]
-            keys_v = [f("v_pre")[p0:row + 1]]
+            kk = f("k_pre", slice(p0, last + 1))
+            vv = f("v_pre", slice(p0, last + 1))
             n_members = int(group_sizes[g])
             copies = max(1, n_members)
             share = 1.0 / n_members if n_members else 1.0
-            qrow, dorow = f("q_pre")[row], (f("do_pre")[row] if grads else None)
+            limit = {a: rows[a] - p0 + 1 for a in members}  # keys seen by the row
+            qn, don = "q_pre", "do_pre"
         else:
-            m = _member_of(cu_s, row)
+            m = idx
             g = _group_of_member(group_sizes, m)
             p0, p1 = int(cu_p[g]), int(cu_p[g + 1])
             s0 = int(cu_s[m])
-            keys_k = [f("k_pre")[p0:p1], f("k_suf")[s0:row + 1]]
-            keys_v = [f("v_pre")[p0:p1], f("v_suf")[s0:row + 1]]
+            kk = np.concatenate([f("k_pre", slice(p0, p1)), f("k_suf", slice(s0, last + 1))], axis=0)
+            vv = np.concatenate([f("v_pre", slice(p0, p1)), f("v_suf", slice(s0, last + 1))], axis=0)
             copies, share = 1, 1.0
-            qrow, dorow = f("q_suf")[row], (f("do_suf")[row] if grads else None)
-        kk = np.concatenate(keys_k, axis=0).astype(dtype)
-        vv = np.concatenate(keys_v, axis=0).astype(dtype)
-        for b, h in enumerate(heads):
-            kv = _kv_head(h, h_q, h_kv)
-            qv = qrow[h].astype(dtype)
-            z = scale * (kk[:, kv, :] @ qv)
-            mx = z.max()
-            l_ = mx + np.log(np.exp(z - mx).sum())
-            p = np.exp(z - l_)
-            o[a, b] = p @ vv[:, kv, :]
-            lse[b, a] = l_
-            if grads:
-                acc = np.zeros(d, dtype)
-                for _ in range(copies):
-                    dov = dorow[h].astype(dtype) * dtype(share)
-                    da = vv[:, kv, :] @ dov
-                    dz = p * (da - (p * da).sum())
-                    acc += scale * (dz @ kk[:, kv, :])
-                dq[a, b] = acc
+            limit = {a: (p1 - p0) + rows[a] - s0 + 1 for a in members}
+            qn, don = "q_suf", "do_suf"
+        ridx = [rows[a] for a in members]
+        qsel = f(qn, ridx)  # [rows, h_q, d]
+        dosel = f(don, ridx) if grads else None
+        for kv in sorted(set(_kv_head(h, h_q, h_kv) for h in heads)):
+            hb = [b for b, h in enumerate(heads) if _kv_head(h, h_q, h_kv) == kv]
+            # query vectors of this kv head: (row a, head b) pairs
+            pairs = [(i, b) for i in range(len(members)) for b in hb]
+            for c0 in range(0, len(pairs), batch):
+                part = pairs[c0:c0 + batch]
+                qm = np.stack([qsel[i, heads[b]] for i, b in part])
+                lim = np.array([limit[members[i]] for i, _ in part])[:, None]
+                z = scale * (qm @ kk[:, kv, :].T)
+                z = np.where(np.arange(kk.shape[0])[None, :] < lim, z, -np.inf)
+                mx = z.max(axis=1, keepdims=True)
+                l_ = mx + np.log(np.exp(z - mx).sum(axis=1, keepdims=True))
+                p = np.exp(z - l_)
+                om = p @ vv[:, kv, :]
+                if grads:
+                    dom = np.stack([dosel[i, heads[b]] for i, b in part]) * dtype(share)
+                    da = dom @ vv[:, kv, :].T
+                    dz = p * (da - (p * da).sum(axis=1, keepdims=True))
+                    dqm = scale * (dz @ kk[:, kv, :]) * dtype(copies)
+                for j, (i, b) in enumerate(part):
+                    a = members[i]
+                    o[a, b] = om[j]
+                    lse[b, a] = l_[j, 0]
+                    if grads:
+                        dq[a, b] = dqm[j]
     out = {"o": o, "lse": lse}
     if grads:
         out["dq"] = dq
@@ -292,8 +316,10 @@ def key_gradients(prefix_lens, group_sizes, suffix_lens, t, scale, group, kv_hea
     vp = np.asarray(t["v_pre"][p0:p1, kv_head, :], dtype)
 
     def accumulate(q, do, k, v, first_row, n_rows, cols):
-        # rows first_row .. first_row+n_rows-1 of a sequence whose key j is k[j]; row r sees keys 0..r
-        for r0 in range(first_row, first_row + n_rows, chunk):
+        # rows first_row .. first_row+n_rows-1 of a sequence whose key j is k[j]; row r sees keys 0..r.
+        # Rows before the first selected key see none of them and are not evaluated.
+        start = max(first_row, min(c for _, c in cols))
+        for r0 in range(start, first_row + n_rows, chunk):
             r1 = min(first_row + n_rows, r0 + chunk)
             z = scale * (q[r0 - first_row:r1 - first_row] @ k[:r1].T)
             rows = np.arange(r0, r1)[:, None]

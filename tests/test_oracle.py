@@ -260,3 +260,52 @@ def test_causal_attention_chunking_is_exact():
     b = causal_attention(q, k[:, :1], v[:, :1], 0.5, do=do, split=None, chunk=100)
     for key in a:
         np.testing.assert_allclose(a[key], b[key], atol=1e-13)
+
+
+SAMPLED_CASES = [
+    # (prefix, groups, suffix, h_q, h_kv): P = 0, empty members, G = 1, an empty group, several groups and
+    # kv heads, GQA ratios 1, 2, 3
+    ((0,), (3,), (4, 2, 5), 2, 1),
+    ((6,), (1,), (5,), 4, 2),
+    ((5, 4), (3, 2), (3, 0, 4, 2, 1), 6, 2),
+    ((3, 0, 7), (2, 2, 1), (2, 3, 1, 4, 3), 3, 3),
+    ((4, 5), (0, 2), (3, 2), 4, 1),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SAMPLED_CASES)))
+def test_sampled_oracles_match_packed_autograd(case, torch_cpu):
+    """query_rows and key_gradients (the oracles of the full-size checks, which evaluate each distinct query
+    row once with the whole dO_pre, Lemma 1) against the independent Eq. (2) masked formulation whose
+    gradients come from torch autograd: every row, every head, every key of every group and kv head."""
+    prefix, groups, suffix, hq, hkv = SAMPLED_CASES[case]
+    prob, t = small(prefix, groups, suffix, h_q=hq, h_kv=hkv, d=8, seed=40 + case)
+    ref = packed_masked(torch_cpu, prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale)
+    args = (prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale)
+    heads = list(range(hq))
+    for side, n in (("pre", prob.total_prefix), ("suf", prob.total_suffix)):
+        if n == 0:
+            continue
+        rows = list(range(n))
+        r = query_rows(*args, side, rows, heads, batch=5)
+        np.testing.assert_allclose(r["o"], ref["o_" + side], atol=1e-12)
+        np.testing.assert_allclose(r["dq"], ref["dq_" + side], atol=1e-12)
+    cu_p, cu_s = prob.cu_prefix, prob.cu_suffix
+    m = 0
+    for g, (p, gs) in enumerate(zip(prob.prefix_lens, prob.group_sizes)):
+        pkeys = list(range(int(cu_p[g]), int(cu_p[g + 1])))
+        skeys = list(range(int(cu_s[m]), int(cu_s[m + gs])))
+        m += int(gs)
+        for kv in range(hkv):
+            for side, keys in (("pre", pkeys), ("suf", skeys)):
+                if not keys:
+                    continue
+                r = key_gradients(*args, g, kv, side, keys, chunk=3)
+                np.testing.assert_allclose(r["dk"], ref["dk_" + side][keys, kv], atol=1e-12)
+                np.testing.assert_allclose(r["dv"], ref["dv_" + side][keys, kv], atol=1e-12)
+    # a key subset in any order gives the same per-key values
+    if prob.total_prefix > 2:
+        keys = [int(cu_p[1]) - 1, int(cu_p[0])] if len(prob.prefix_lens) else []
+        if keys and keys[0] > keys[1]:
+            r = key_gradients(*args, 0, 0, "pre", keys, chunk=2)
+            np.testing.assert_allclose(r["dk"], ref["dk_pre"][keys, 0], atol=1e-12)
