@@ -3,8 +3,13 @@
 Tolerances (per tensor):
 * fp32 workloads: max |gpu - oracle| <= 1e-4 for outputs, log-sum-exp and gradients;
 * bf16 workloads: outputs and log-sum-exp max |gpu - oracle| <= 2e-2; gradients
-  max |gpu - oracle| / max |oracle| <= 3e-2.
-The oracle runs in float64 on exactly the (bf16-rounded) inputs the GPU sees.
+  max |gpu - oracle| / max |oracle| <= 3e-2;
+* bf16 workloads, every tensor, also ||gpu - oracle||_2 / ||oracle||_2 <= 1e-2: at long
+  context |O| is ~0.01-0.02, so the absolute bound alone would pass an output off by half
+  its size; rounding the operands and results to bf16 (relative 2^-9 each) keeps the
+  norm-relative error near 3e-3.
+The oracle runs in float64 (float32 for the full-size sampled checks) on exactly the
+(bf16-rounded) inputs the GPU sees.
 """
 import sys
 
@@ -15,6 +20,7 @@ from paper_2506_05433_amd.inputs import bf16_bits_to_f32
 FP32_ABS = 1e-4
 BF16_OUT_ABS = 2e-2
 BF16_GRAD_REL = 3e-2
+BF16_NORM_REL = 1e-2
 
 OUTS = ("o_pre", "o_suf", "lse_pre", "lse_suf")
 GRADS = ("dq_pre", "dk_pre", "dv_pre", "dq_suf", "dk_suf", "dv_suf")
@@ -49,20 +55,24 @@ def to_host(t):
 
 
 def report(name, got, ref):
+    """(max |gpu - ref|, that / max |ref|, ||gpu - ref||_2 / ||ref||_2)."""
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
     if ref.size == 0:
-        return 0.0, 0.0
-    err = float(np.abs(got - ref).max())
+        return 0.0, 0.0, 0.0
+    diff = got - ref
+    err = float(np.abs(diff).max())
     scale = float(np.abs(ref).max())
-    return err, err / scale if scale > 0 else err
+    nref = float(np.sqrt((ref * ref).sum()))
+    nrel = float(np.sqrt((diff * diff).sum())) / nref if nref > 0 else float(np.sqrt((diff * diff).sum()))
+    return err, (err / scale if scale > 0 else err), nrel
 
 
 def check(name, got, ref, dtype, log=None):
     """Assert ``got`` matches ``ref`` under the tolerance for tensor ``name`` in ``dtype`` mode."""
     assert got.shape == ref.shape, (name, got.shape, ref.shape)
     assert np.all(np.isfinite(got)), f"{name}: non-finite values"
-    err, rel = report(name, got, ref)
+    err, rel, nrel = report(name, got, ref)
     grad = name.startswith("d")
     if dtype == "fp32":
         ok, bound, val = err <= FP32_ABS, FP32_ABS, err
@@ -70,7 +80,10 @@ def check(name, got, ref, dtype, log=None):
         ok, bound, val = rel <= BF16_GRAD_REL, BF16_GRAD_REL, rel
     else:
         ok, bound, val = err <= BF16_OUT_ABS, BF16_OUT_ABS, err
-    msg = f"{name}: max_abs={err:.3e} max_rel={rel:.3e} (bound {bound:g})"
+    if dtype != "fp32":
+        ok = ok and nrel <= BF16_NORM_REL
+    msg = f"{name}: max_abs={err:.3e} max_rel={rel:.3e} norm_rel={nrel:.3e} (bound {bound:g}" + \
+        (f", norm {BF16_NORM_REL:g})" if dtype != "fp32" else ")")
     if log is not None:
         log.append(msg)
     print(msg, file=sys.stderr)

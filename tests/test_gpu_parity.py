@@ -101,6 +101,11 @@ SMALL = [
     (((3, 0, 200, 1), (2, 1, 0, 3), (5, 0, 7, 1, 1, 130)), 8, 1, 128, "bf16"),
     # GQA ratio 5 with head_dim 64
     (((150,), (2,), (77, 200)), 5, 1, 64, "bf16"),
+    # the head geometries of the full-size workloads (8 kv heads: the XCD head-mapping branch that gives
+    # each XCD one kv head), every element of every head
+    (((300,), (3,), (130, 64, 200)), 32, 8, 128, "bf16"),
+    (((257,), (3,), (100, 1, 190)), 40, 8, 128, "bf16"),
+    (((200, 130), (2, 2), (70, 129, 5, 60)), 64, 8, 128, "bf16"),
 ]
 
 
@@ -135,63 +140,125 @@ def test_peaked_softmax_rescaling():
     _full_compare(prob)
 
 
-def test_single_group_workload_kv_head0():
-    """single_group (P=4096, G=8, 32/8 heads) at full size; every element of query heads 0-3 and kv head 0."""
+def test_single_group_workload_every_head():
+    """single_group (P=4096, G=8, 32/8 heads) at full size: every element of every head."""
     prob = make_problem("single_group", seed=0)
-    _full_compare(prob, heads=[0, 1, 2, 3], kv_heads=[0])
+    _full_compare(prob, heads=list(range(prob.h_q)))
 
 
-def _sampled_compare(prob, n_rows=12, n_keys=6, heads=None, kv_head=0, group=0, seed=0):
+def _tiles(lo, hi, bm=128):
+    """(first row, last row) of every bm-row tile of [lo, hi) (the planner's query tiles)."""
+    return [(a, min(a + bm, hi) - 1) for a in range(lo, hi, bm)]
+
+
+def _identities(prob, got_dev, dev):
+    """Over every group and kv head, on the GPU's own results: sum of dV over the group's keys = sum of dO
+    over the group's queries and the kv head's query heads (softmax rows sum to one), and sum of dK = 0
+    (every row of dS sums to zero), relative to sum |dK|."""
+    ratio = prob.h_q // prob.h_kv
+    cu_p, cu_s = prob.cu_prefix, prob.cu_suffix
+    m = 0
+    worst_v = worst_k = 0.0
+    for g, gs in enumerate(prob.group_sizes):
+        p0, p1 = int(cu_p[g]), int(cu_p[g + 1])
+        s0, s1 = int(cu_s[m]), int(cu_s[m + int(gs)])
+        m += int(gs)
+        if p1 == p0 and s1 == s0:
+            continue
+
+        def seg(t, a, b):
+            return t[a:b].double().sum(0)
+
+        dv = seg(got_dev["dv_pre"], p0, p1) + seg(got_dev["dv_suf"], s0, s1)            # [h_kv, d]
+        do = seg(dev["do_pre"], p0, p1) + seg(dev["do_suf"], s0, s1)                    # [h_q, d]
+        do = do.view(prob.h_kv, ratio, -1).sum(1)
+        dk = seg(got_dev["dk_pre"], p0, p1) + seg(got_dev["dk_suf"], s0, s1)
+        dk_abs = got_dev["dk_pre"][p0:p1].double().abs().sum(0) + got_dev["dk_suf"][s0:s1].double().abs().sum(0)
+        rv = float(((dv - do).abs().amax(1) / do.abs().amax(1).clamp_min(1e-30)).max())
+        assert bool((dk_abs.amax(1) > 0).all()), f"group {g}: a kv head has all-zero dK"
+        rk = float((dk.abs().amax(1) / dk_abs.amax(1)).max())
+        worst_v, worst_k = max(worst_v, rv), max(worst_k, rk)
+    print(f"identities over {len(prob.group_sizes)} groups x {prob.h_kv} kv heads: "
+          f"sum dV vs sum dO rel={worst_v:.3e}; |sum dK| / sum |dK| = {worst_k:.3e}", flush=True)
+    assert worst_v < 3e-2 and worst_k < 1e-2
+
+
+def _sampled_compare(prob, head_groups=1, kv_group=0, kv_heads=None, n_keys=4, seed=0):
+    """Full-size workload against the oracle on sampled outputs, float32 oracle.
+
+    * query side: the first and last row of every query tile (prefix tiles of every group, response
+      tiles stacked over the members of every group), every query head (with ``head_groups`` > 1, tile i
+      takes the heads h with h % head_groups == i % head_groups, so every head and every tile is covered);
+      O, LSE and dQ;
+    * key side: dK, dV of keys of group ``kv_group`` for every kv head in ``kv_heads`` (default all):
+      the last prefix keys (where the causal prefix rows end), a few random prefix keys near the end, the
+      first and last response keys of the first and last member, and random response keys;
+    * the sum identities over every group and kv head.
+    """
     print(f"[parity] sampled {prob.workload.name} seed={prob.seed} total_prefix={prob.total_prefix} "
           f"total_suffix={prob.total_suffix}", flush=True)
-    got = _run(prob)
+    binding = _dev()
+    dev = binding.to_device(prob, "cuda")
+    f = binding.run_fwd(dev)
+    g = binding.run_bwd(dev, f)
+    torch.cuda.synchronize()
+    got_dev = dict(zip(OUTS, f))
+    got_dev.update(zip(GRADS, g))
+    _identities(prob, got_dev, dev)
     t = host_view(prob)
     rng = np.random.default_rng(seed)
     hq = prob.h_q
-    heads = heads if heads is not None else [0, hq // 2 + 1, hq - 1]
     cu_p, cu_s = prob.cu_prefix, prob.cu_suffix
-    pre_rows = sorted(set([0, 127, 128, int(cu_p[1]) - 1] + list(rng.integers(0, prob.total_prefix, n_rows))))
-    suf_rows = sorted(set([0, int(cu_s[1]) - 1, int(cu_s[1]), prob.total_suffix - 1] +
-                          list(rng.integers(0, prob.total_suffix, n_rows))))
-    for side, rows in (("pre", pre_rows), ("suf", suf_rows)):
-        r = query_rows(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, side, rows, heads)
-        check("o_" + side, got["o_" + side][rows][:, heads], r["o"], prob.dtype)
-        check("lse_" + side, got["lse_" + side][heads][:, rows], r["lse"], prob.dtype)
-        check("dq_" + side, got["dq_" + side][rows][:, heads], r["dq"], prob.dtype)
-    p0, p1 = int(cu_p[group]), int(cu_p[group + 1])
-    m0 = int(prob.group_sizes[:group].sum())
-    m1 = m0 + int(prob.group_sizes[group])
-    pkeys = sorted(set([p0, p1 - 1, min(p0 + 128, p1 - 1)] + list(rng.integers(p0, p1, n_keys))))
-    skeys = sorted(set([int(cu_s[m0]), int(cu_s[m1]) - 1] + list(rng.integers(cu_s[m0], cu_s[m1], n_keys))))
-    for side, keys in (("pre", pkeys), ("suf", skeys)):
-        r = key_gradients(prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale, group, kv_head, side,
-                          keys)
-        # relative bound against the sampled reference's own max, plus the full tensor's scale
-        check("dk_" + side, got["dk_" + side][keys, kv_head], r["dk"], prob.dtype)
-        check("dv_" + side, got["dv_" + side][keys, kv_head], r["dv"], prob.dtype)
-    # identities over every key of group 0 / kv head 0 (any size): sum dK = 0, sum dV = sum dO
-    s0, s1 = int(cu_s[m0]), int(cu_s[m1])
-    hs = [h for h in range(hq) if h // (hq // prob.h_kv) == kv_head]
-    dv_sum = got["dv_pre"][p0:p1, kv_head].astype(np.float64).sum(0) + got["dv_suf"][s0:s1, kv_head].sum(0)
-    do_sum = np.asarray(t["do_pre"][p0:p1], np.float64)[:, hs].sum((0, 1)) + \
-        np.asarray(t["do_suf"][s0:s1], np.float64)[:, hs].sum((0, 1))
-    rel = np.abs(dv_sum - do_sum).max() / np.abs(do_sum).max()
-    print(f"sum dV vs sum dO rel={rel:.3e}", flush=True)
-    assert rel < 3e-2
+    args = (prob.prefix_lens, prob.group_sizes, prob.suffix_lens, t, prob.scale)
+    m = 0
+    pre_tiles, suf_tiles = [], []
+    for gi, gs in enumerate(prob.group_sizes):
+        pre_tiles += _tiles(int(cu_p[gi]), int(cu_p[gi + 1]))
+        suf_tiles += _tiles(int(cu_s[m]), int(cu_s[m + int(gs)]))
+        m += int(gs)
+    for side, tiles in (("pre", pre_tiles), ("suf", suf_tiles)):
+        for hg in range(head_groups):
+            heads = [h for h in range(hq) if h % head_groups == hg]
+            rows = sorted(set(r for i, tr in enumerate(tiles) if i % head_groups == hg for r in tr))
+            if not rows:
+                continue
+            r = query_rows(*args, side, rows, heads, dtype=np.float32)
+            idx_r = torch.tensor(rows, device="cuda")
+            idx_h = torch.tensor(heads, device="cuda")
+            check("o_" + side, to_host(got_dev["o_" + side][idx_r][:, idx_h]), r["o"], prob.dtype)
+            check("lse_" + side, to_host(got_dev["lse_" + side][idx_h][:, idx_r]), r["lse"], prob.dtype)
+            check("dq_" + side, to_host(got_dev["dq_" + side][idx_r][:, idx_h]), r["dq"], prob.dtype)
+    gq = kv_group
+    p0, p1 = int(cu_p[gq]), int(cu_p[gq + 1])
+    m0 = int(prob.group_sizes[:gq].sum())
+    m1 = m0 + int(prob.group_sizes[gq])
+    tail = max(p0, p1 - 300)
+    pkeys = sorted(set([p1 - 1, p1 - 2, max(p0, p1 - 129)] + list(rng.integers(tail, p1, n_keys))))
+    skeys = sorted(set([int(cu_s[m0]), int(cu_s[m0 + 1]) - 1, int(cu_s[m1 - 1]), int(cu_s[m1]) - 1] +
+                       list(rng.integers(cu_s[m0], cu_s[m1], n_keys))))
+    for kv in (range(prob.h_kv) if kv_heads is None else kv_heads):
+        for side, keys in (("pre", pkeys), ("suf", skeys)):
+            r = key_gradients(*args, gq, kv, side, keys, dtype=np.float32)
+            idx = torch.tensor(keys, device="cuda")
+            check(f"dk_{side}[kv{kv}]", to_host(got_dev["dk_" + side][idx, kv]), r["dk"], prob.dtype)
+            check(f"dv_{side}[kv{kv}]", to_host(got_dev["dv_" + side][idx, kv]), r["dv"], prob.dtype)
 
 
 def test_long_prefix_workload_sampled():
+    """long_prefix (P=16384, G=16, 32/8): every tile, every head; dK/dV of every kv head."""
     _sampled_compare(make_problem("long_prefix", seed=0))
 
 
 def test_large_group_workload_sampled():
-    _sampled_compare(make_problem("large_group", seed=0))
+    """large_group (P=8192, G=64, 40/8): every tile, every head; dK/dV of kv heads 0 and 7."""
+    _sampled_compare(make_problem("large_group", seed=0), kv_heads=[0, 7])
 
 
 def test_packed_varlen_workload_sampled():
+    """packed_varlen (8 groups, 64/8): every tile with 8 of its heads (every head over eight tiles in
+    turn); dK/dV of every kv head of the group with the shortest prefix."""
     prob = make_problem("packed_varlen", seed=0)
-    g = int(np.argmin(prob.prefix_lens))
-    _sampled_compare(prob, group=g, kv_head=3)
+    _sampled_compare(prob, head_groups=8, kv_group=int(np.argmin(prob.prefix_lens)))
 
 
 def test_deterministic():
