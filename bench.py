@@ -384,7 +384,7 @@ def cpu_baseline(prob, budget_s):
             "seconds": round(total_s, 2), "host_cpus": len(os.sched_getaffinity(0))}
 
 
-ATTN_SOURCES = ("pg_attn.hip", "pg_bwd.hpp", "pg_common.hpp", "pg_fwd.hpp", "pg_plan.hpp")
+ATTN_SOURCES = ("pg_attn.hip", "pg_bwd.hpp", "pg_common.hpp", "pg_fwd.hpp", "pg_plan.hpp", "pg_types.hpp")
 
 
 def kernel_source_sha():

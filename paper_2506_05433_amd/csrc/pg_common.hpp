@@ -14,6 +14,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "pg_types.hpp"
+
 namespace pg {
 
 typedef __bf16 bf16;
@@ -26,22 +28,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-
-// Tile descriptor produced by the planner.
-//  q tiles : kind 0 = prefix query rows [row0,row1) of group `group` (packed prefix index);
-//            kind 1 = response query rows [row0,row1) (packed suffix index), which may span
-//                     several members of the group; aux = first response key any row sees
-//                     (start of the member that owns row0).
-//  kv tiles: kind 0 = prefix keys [row0,row1); kind 1 = response keys [row0,row1);
-//            aux = end of the response rows that can see them (end of the member owning row1-1).
-struct TileDesc {
-  int kind, group, row0, row1, aux, work, chunk, nchunks;
-};
-
-// Per-group ranges: prefix rows [p0,p1), response rows [s0,s1).
-struct GroupInfo {
-  int p0, p1, s0, s1;
-};
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
@@ -67,55 +53,6 @@ __device__ __forceinline__ float wave_swap32_sum(float v) {
   float a, b;
   swap_halves(v, a, b);
   return a + b;
-}
-
-// ---------------------------------------------------------------- XCD-aware block order
-// MI355X has 8 XCDs with a private L2 each, and workgroup ids are handed to them
-// round-robin (id % 8). Grids are ordered so that the workgroups that read the same
-// key/value head run on the same XCD: with `units` work units (tiles, longest first)
-// and `heads` heads per unit, of which `per_kv` consecutive heads share a kv head,
-// block b of xcd = b % 8 takes the j-th (b / 8) slot of that XCD. When the number of
-// kv heads is a multiple of 8, XCD x owns kv heads x, x+8, ...; when it divides 8,
-// each kv head is spread over 8 / n_kv XCDs. Otherwise the plain order is used.
-// Slots past the end map to unit >= units (the block exits).
-constexpr int kXcds = 8;
-
-struct BlockSlot {
-  int unit, head;
-};
-
-__host__ __device__ inline long xcd_grid_blocks(long units, int heads, int per_kv) {
-  const int n_kv = heads / per_kv;
-  if (n_kv % kXcds == 0) return units * heads;
-  if (kXcds % n_kv == 0) {
-    const long x = kXcds / n_kv;
-    return kXcds * ((units * per_kv + x - 1) / x);
-  }
-  return units * heads;
-}
-
-__device__ __forceinline__ BlockSlot xcd_slot(int b, int heads, int per_kv) {
-  const int n_kv = heads / per_kv;
-  BlockSlot s;
-  if (n_kv % kXcds == 0) {
-    const int xcd = b % kXcds, j = b / kXcds;
-    const int per_xcd = heads / kXcds;  // heads owned by one XCD
-    s.unit = j / per_xcd;
-    const int sub = j % per_xcd;
-    const int kv = xcd + kXcds * (sub / per_kv);
-    s.head = kv * per_kv + sub % per_kv;
-  } else if (kXcds % n_kv == 0) {
-    const int xcd = b % kXcds, j = b / kXcds;
-    const int x = kXcds / n_kv;
-    const int kv = xcd % n_kv, part = xcd / n_kv;
-    const int p = j * x + part;
-    s.unit = p / per_kv;
-    s.head = kv * per_kv + p % per_kv;
-  } else {
-    s.unit = b / heads;
-    s.head = b % heads;
-  }
-  return s;
 }
 
 // ---------------------------------------------------------------- LDS tile addressing

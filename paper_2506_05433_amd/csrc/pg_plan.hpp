@@ -9,7 +9,9 @@
 // the per-member causal mask. Key/value tiles are the mirror image for the
 // key-stationary gradient kernel.
 #pragma once
-#include "pg_common.hpp"
+#include <hip/hip_runtime.h>
+
+#include "pg_types.hpp"
 
 namespace pg {
 
@@ -25,18 +27,18 @@ struct GroupInfoEx {
 };
 
 // Inclusive scan of one value per thread over a block of NT threads.
-template <int NT>
-__device__ __forceinline__ int block_inclusive_scan(int v, int* tmp) {
+template <int NT, typename V>
+__device__ __forceinline__ V block_inclusive_scan(V v, V* tmp) {
   const int t = threadIdx.x;
   tmp[t] = v;
   __syncthreads();
   for (int off = 1; off < NT; off <<= 1) {
-    int add = (t >= off) ? tmp[t - off] : 0;
+    V add = (t >= off) ? tmp[t - off] : 0;
     __syncthreads();
     tmp[t] += add;
     __syncthreads();
   }
-  int r = tmp[t];
+  V r = tmp[t];
   __syncthreads();
   return r;
 }
@@ -57,6 +59,8 @@ constexpr int kPlanThreads = 1024;
 // Shared memory of the one-block planner steps.
 struct PlanShared {
   int tmp[kPlanThreads];
+  long long tmp64[kPlanThreads];
+  long long members;  // running sum of group sizes
   int err;
   int carry[3];
 };
@@ -70,7 +74,7 @@ __device__ inline void plan_groups_body(const int* __restrict__ cu_p, const int*
   int& err = sh.err;
   int* carry = sh.carry;
   const int t = threadIdx.x;
-  if (t == 0) { err = 0; carry[0] = carry[1] = carry[2] = 0; }
+  if (t == 0) { err = 0; carry[0] = carry[1] = carry[2] = 0; sh.members = 0; }
   __syncthreads();
   int bad = 0;
   for (int g = t; g <= ng; g += kPlanThreads) {
@@ -78,7 +82,7 @@ __device__ inline void plan_groups_body(const int* __restrict__ cu_p, const int*
     if (g == 0 && v != 0) bad = 1;
     if (g == ng && v != tp) bad = 1;
     if (g > 0 && v < cu_p[g - 1]) bad = 1;
-    if (g < ng && gsz[g] < 0) bad = 1;
+    if (g < ng && (gsz[g] < 0 || gsz[g] > ns)) bad = 1;
   }
   for (int m = t; m <= ns; m += kPlanThreads) {
     int v = cu_s[m];
@@ -88,17 +92,20 @@ __device__ inline void plan_groups_body(const int* __restrict__ cu_p, const int*
   }
   if (bad) atomicOr(&err, 1);
   __syncthreads();
-  // member starts: exclusive scan of group sizes (checked against ns afterwards)
+  // member starts: exclusive scan of group sizes, in 64 bits so that no sum of sizes can wrap
+  // around to n_suffixes; checked against it afterwards, and only then are the starts used to
+  // index cu_suffix_lens
   for (int base = 0; base < ng; base += kPlanThreads) {
     const int g = base + t;
-    const int v = (g < ng && !err) ? gsz[g] : 0;
-    const int inc = block_inclusive_scan<kPlanThreads>(v, tmp);
-    if (g < ng) { ginfo[g].m0 = carry[0] + inc - v; ginfo[g].m1 = carry[0] + inc; }
+    const long long v = (g < ng && !err) ? gsz[g] : 0;
+    const long long inc = block_inclusive_scan<kPlanThreads>(v, sh.tmp64);
+    const long long m1 = sh.members + inc;
+    if (g < ng) { ginfo[g].m0 = (int)(m1 - v); ginfo[g].m1 = (int)m1; }
     __syncthreads();
-    if (t == kPlanThreads - 1) carry[0] += inc;
+    if (t == kPlanThreads - 1) sh.members = m1;
     __syncthreads();
   }
-  if (t == 0 && carry[0] != ns) err = 1;
+  if (t == 0 && sh.members != ns) err = 1;
   __syncthreads();
   const int ok = !err;
   for (int base = 0; base < ng; base += kPlanThreads) {

@@ -13,6 +13,7 @@
 // streaming read and write of q and k, so the kernel is HBM-bound; rows are
 // read and written in 16-byte (bf16) or 32-byte (fp32) chunks of 8 elements.
 #pragma once
+#include "pg_common.hpp"
 #include "pg_plan.hpp"
 
 namespace pg {
