@@ -65,18 +65,19 @@ Layout make_layout(int ng, int ns, int tp, int ts, int h_q, int h_kv, int d, boo
   L.max_kv = bwd ? (ceil_div_l(tp, pg::kKvBN) + ng) * L.kv_chunks + ceil_div_l(ts, pg::kKvBN) + ng : 0;
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
+  const size_t rows = (size_t)tp + (size_t)ts;  // sizes are non-negative ints: no overflow in 64 bits
   L.hdr = take(sizeof(pg::PlanHeader));
   L.ginfo = take(sizeof(pg::GroupInfoEx) * (size_t)(ng > 0 ? ng : 1));
-  L.qoff = take(sizeof(int) * (size_t)(ng + 1));
-  L.kvoff = take(sizeof(int) * (size_t)(ng + 1));
+  L.qoff = take(sizeof(int) * ((size_t)ng + 1));
+  L.kvoff = take(sizeof(int) * ((size_t)ng + 1));
   L.qtiles = take(sizeof(pg::TileDesc) * (size_t)(L.max_q > 0 ? L.max_q : 1));
   L.qorder = take(sizeof(int) * (size_t)(L.max_q > 0 ? L.max_q : 1));
   L.kvtiles = take(sizeof(pg::TileDesc) * (size_t)(L.max_kv > 0 ? L.max_kv : 1));
   L.kvorder = take(sizeof(int) * (size_t)(L.max_kv > 0 ? L.max_kv : 1));
   L.seg = take(sizeof(int) * (size_t)(ts > 0 ? ts : 1));
-  L.dsum = bwd ? take(sizeof(float) * (size_t)h_q * (size_t)(tp + ts > 0 ? tp + ts : 1)) : off;
-  L.part = (bwd && L.kv_chunks > 1) ? take(sizeof(float) * (size_t)L.kv_chunks * 2 * tp * h_kv * d) : off;
-  L.xrow = bwd ? take(sizeof(int) * (size_t)(tp + ts > 0 ? tp + ts : 1)) : off;
+  L.dsum = bwd ? take(sizeof(float) * (size_t)h_q * (rows > 0 ? rows : 1)) : off;
+  L.part = (bwd && L.kv_chunks > 1) ? take(sizeof(float) * (size_t)L.kv_chunks * 2 * (size_t)tp * h_kv * d) : off;
+  L.xrow = bwd ? take(sizeof(int) * (rows > 0 ? rows : 1)) : off;
   L.total = off;
   return L;
 }
@@ -377,8 +378,8 @@ LastLayout last_layout(int ng, int ns, int h_q, int h_kv, int d) {
   auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
   L.hdr = take(sizeof(pg::PlanHeader));
   L.ginfo = take(sizeof(pg::GroupInfoEx) * (size_t)(ng > 0 ? ng : 1));
-  L.qoff = take(sizeof(int) * (size_t)(ng + 1));
-  L.kvoff = take(sizeof(int) * (size_t)(ng + 1));
+  L.qoff = take(sizeof(int) * ((size_t)ng + 1));
+  L.kvoff = take(sizeof(int) * ((size_t)ng + 1));
   L.blocks = take(sizeof(pg::LastBlock) * (size_t)(L.nb_max > 0 ? L.nb_max : 1));
   L.nblk = take(sizeof(int));
   const size_t slots = (size_t)(L.nb_max > 0 ? L.nb_max : 1) * (h_kv > 0 ? h_kv : 1) * L.nch * pg::kLastRows;
@@ -400,8 +401,8 @@ RopeLayout rope_layout(int ng) {
   auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
   L.hdr = take(sizeof(pg::PlanHeader));
   L.ginfo = take(sizeof(pg::GroupInfoEx) * (size_t)(ng > 0 ? ng : 1));
-  L.qoff = take(sizeof(int) * (size_t)(ng + 1));
-  L.kvoff = take(sizeof(int) * (size_t)(ng + 1));
+  L.qoff = take(sizeof(int) * ((size_t)ng + 1));
+  L.kvoff = take(sizeof(int) * ((size_t)ng + 1));
   L.total = off;
   return L;
 }
