@@ -101,6 +101,30 @@ int pg_attn_fwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int t
                 void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Forward pass without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same computation and the same kernels as
+ * pg_attn_fwd, bitwise the same results, with the tile plan kept in a scratch
+ * array of PG_NOALLOC_SCRATCH_BYTES that the library holds in each device's
+ * memory until the process ends. The call allocates nothing (no hipMalloc,
+ * no library allocation); on a device's first call it looks up that device's
+ * copy of the array. Problems whose plan needs more than
+ * pg_attn_fwd_workspace_size() <= PG_NOALLOC_SCRATCH_BYTES bytes are rejected
+ * with PG_EUNSUPPORTED before anything is launched (16 MiB holds the plan of
+ * about four million response rows). Every call on one device shares that
+ * device's array: calls that overlap in time on one device (other streams,
+ * other threads) race and must not be issued. Arguments, layout, ownership
+ * and the other errors are those of pg_attn_fwd.
+ */
+#define PG_NOALLOC_SCRATCH_BYTES (16u << 20)
+int pg_attn_fwd_noalloc(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                        const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                        int h_q, int h_kv, int head_dim, float softmax_scale,
+                        const void* q_pre, const void* k_pre, const void* v_pre,
+                        const void* q_suf, const void* k_suf, const void* v_suf,
+                        void* o_pre, void* o_suf, float* lse_pre, float* lse_suf, void* stream);
+
+/*
  * Backward pass: the vector-Jacobian product of the forward with upstream
  * gradients do_pre, do_suf (Lemma 1 and its proof, Appendix A.1). dq/dk/dv of
  * the suffix rows are those of each member's own rows; dq_pre, dk_pre, dv_pre

@@ -26,6 +26,7 @@ SIGNATURES = {
     "pg_attn_bwd_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
     "pg_attn_fwd": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 10 + [_P, _Z, _P]),
     "pg_attn_bwd": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 18 + [_P, _Z, _P]),
+    "pg_attn_fwd_noalloc": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 10 + [_P]),
     "pg_attn_fwd_xours": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 5 + [_P, _Z, _P]),
     "pg_attn_bwd_xours": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _I, _F] + [_P] * 9 + [_P, _Z, _P]),
     "pg_attn_fwd_last_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
@@ -203,6 +204,26 @@ def bwd(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, o_pre, o_suf, lse_pre, lse_suf
         _ptr(o_pre), _ptr(o_suf), _ptr(lse_pre), _ptr(lse_suf), _ptr(do_pre), _ptr(do_suf),
         *[_ptr(t) for t in out],
         _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(torch, dev))
+    _check(st)
+    return out
+
+
+def fwd_noalloc(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, cu_prefix, cu_suffix, group_sizes, scale, out):
+    """Forward without a workspace (pg_attn_fwd_noalloc): the plan lives in the library's per-device scratch
+    array. ``out`` = (o_pre, o_suf, lse_pre, lse_suf), preallocated by the caller. Returns ``out``."""
+    import torch
+    ng, ns, tp, ts, hq, hkv, d = _shapes(q_pre, k_pre, q_suf, cu_prefix, cu_suffix, group_sizes)
+    dev, dt = q_pre.device, q_pre.dtype
+    o_pre, o_suf, lse_pre, lse_suf = out
+    _expect(dev, dt, q_pre=((tp, hq, d), q_pre), k_pre=((tp, hkv, d), k_pre), v_pre=((tp, hkv, d), v_pre),
+            q_suf=((ts, hq, d), q_suf), k_suf=((ts, hkv, d), k_suf), v_suf=((ts, hkv, d), v_suf),
+            o_pre=((tp, hq, d), o_pre), o_suf=((ts, hq, d), o_suf), lse_pre=((hq, tp), lse_pre),
+            lse_suf=((hq, ts), lse_suf))
+    st = lib().pg_attn_fwd_noalloc(
+        _dtype_code(torch, dt), ng, ns, tp, ts,
+        _ptr(cu_prefix), _ptr(cu_suffix), _ptr(group_sizes), hq, hkv, d, float(scale),
+        _ptr(q_pre), _ptr(k_pre), _ptr(v_pre), _ptr(q_suf), _ptr(k_suf), _ptr(v_suf),
+        _ptr(o_pre), _ptr(o_suf), _ptr(lse_pre), _ptr(lse_suf), _stream(torch, dev))
     _check(st)
     return out
 

@@ -18,6 +18,12 @@
 #include "pg_last.hpp"
 #include "pg_rope.hpp"
 
+// Scratch of pg_attn_fwd_noalloc: the tile plan that pg_attn_fwd keeps in the caller's
+// workspace. Every device the library runs on holds its own copy until the process ends.
+// In host code `scratch` only names the symbol; its device address comes from
+// hipGetSymbolAddress, once per device (scratch_ptr below).
+__device__ __align__(256) char scratch[PG_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -95,9 +101,11 @@ struct Rec {
 std::mutex mu;
 bool on = false;
 int n = 0;
+thread_local bool suppressed = false;  // set by calls that must not create events
 std::vector<Rec> recs;
 
 int begin(int kernel, hipStream_t st) {
+  if (suppressed) return -1;
   std::lock_guard<std::mutex> g(mu);
   if (!on || n >= kCap) return -1;
   if ((int)recs.size() <= n) {
@@ -159,6 +167,28 @@ int device_ready() {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  return PG_OK;
+}
+
+// Device address of `scratch` on the current device, looked up on the device's first call.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_ptr(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(PG_EUNSUPPORTED, "device id %d (at most %d devices)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(PG_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return PG_OK;
 }
 
@@ -481,6 +511,35 @@ int pg_attn_fwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int t
     return fail(PG_EINVAL, "a suffix tensor pointer is NULL");
   return fwd_impl(c, cu_prefix_lens, cu_suffix_lens, group_sizes, q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, o_pre,
                   o_suf, lse_pre, lse_suf, false, workspace, workspace_bytes, stream);
+}
+
+int pg_attn_fwd_noalloc(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
+                        const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
+                        int h_q, int h_kv, int head_dim, float softmax_scale,
+                        const void* q_pre, const void* k_pre, const void* v_pre,
+                        const void* q_suf, const void* k_suf, const void* v_suf,
+                        void* o_pre, void* o_suf, float* lse_pre, float* lse_suf, void* stream) {
+  g_last_error.clear();
+  const Common c{dtype, n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, softmax_scale};
+  int rc = check_common(c, cu_prefix_lens, cu_suffix_lens, group_sizes);
+  if (rc) return rc;
+  if (total_prefix > 0 && (!q_pre || !k_pre || !v_pre || !o_pre || !lse_pre))
+    return fail(PG_EINVAL, "a prefix tensor pointer is NULL");
+  if (total_suffix > 0 && (!q_suf || !k_suf || !v_suf || !o_suf || !lse_suf))
+    return fail(PG_EINVAL, "a suffix tensor pointer is NULL");
+  const size_t need = make_layout(n_groups, n_suffixes, total_prefix, total_suffix, h_q, h_kv, head_dim, false).total;
+  if (need > (size_t)PG_NOALLOC_SCRATCH_BYTES)
+    return fail(PG_EUNSUPPORTED, "the plan needs %zu bytes of scratch, more than the %u held for pg_attn_fwd_noalloc",
+                need, (unsigned)PG_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((rc = scratch_ptr(&ws))) return rc;
+  // no timing brackets: they may create events
+  const bool was = timing::suppressed;
+  timing::suppressed = true;
+  rc = fwd_impl(c, cu_prefix_lens, cu_suffix_lens, group_sizes, q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, o_pre,
+                o_suf, lse_pre, lse_suf, false, ws, (size_t)PG_NOALLOC_SCRATCH_BYTES, stream);
+  timing::suppressed = was;
+  return rc;
 }
 
 int pg_attn_fwd_xours(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,

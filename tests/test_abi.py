@@ -163,3 +163,12 @@ def test_last_validation_and_workspace():
     assert L.pg_attn_fwd_last(0, 1, 2, 8, 6, p, p, p, 4, 2, 96, 0.125, *[p] * 8, p, 1 << 30, None) == 2
     assert L.pg_attn_fwd_last(0, 1, 2, 8, 6, p, p, p, 256, 1, 128, 0.125, *[p] * 8, p, 1 << 30, None) == 2
     assert L.pg_attn_fwd_last(0, 1, 2, 8, 6, p, p, p, 4, 2, 128, 0.125, *[p] * 8, p, 16, None) == 3
+
+
+def test_noalloc_forward_rejects_plans_beyond_its_scratch():
+    """A plan larger than the scratch array is refused on the host, before any device call."""
+    L = binding.lib()
+    p = ctypes.c_void_p(1)
+    ts = 5_000_000  # the per-row member table alone needs 20 MB
+    st = L.pg_attn_fwd_noalloc(0, 1, 1, 0, ts, p, p, p, 1, 1, 64, 0.125, *[p] * 10, None)
+    assert st == 2 and b"scratch" in L.pg_last_error()
