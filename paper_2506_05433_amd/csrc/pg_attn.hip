@@ -48,27 +48,38 @@ long ceil_div_l(long a, long b) { return (a + b - 1) / b; }
 struct Layout {
   size_t hdr, ginfo, qoff, kvoff, qtiles, qorder, kvtiles, kvorder, seg, dsum, part, xrow, total;
   long max_q, max_kv;
-  int kv_chunks;
+  int kv_chunks, split;
 };
 
 // Pieces each prefix key tile's query walk is split into for the dK/dV kernel: enough
 // workgroups to balance the long prefix walks over the CUs (about 512 prefix pieces, i.e.
 // two per CU), at most 8, and 1 when there are already that many prefix key tiles. More
 // pieces balance better but each adds a full fp32 partial to write and reduce; measured on
-// the single-group and large-group workloads, 512 beats 256 and 1024-4096.
-int kv_chunks_for(int ng, int tp, int h_kv) {
+// the single-group and large-group workloads, 512 beats 256 and 1024-4096. A piece keeps at
+// least 16 query tiles of the average walk (a group's rows, once per query head of the kv
+// head): shorter pieces cost more in their fixed start-up and in the reduce launch than they
+// save.
+int kv_chunks_for(int ng, int tp, int ts, int h_q, int h_kv) {
   if (tp <= 0 || h_kv <= 0) return 1;
   const long tiles = (ceil_div_l(tp, pg::kKvBN) + ng) * (long)h_kv;
-  const long c = ceil_div_l(512, tiles);
+  long c = ceil_div_l(512, tiles);
+  const long walk = ceil_div_l((long)tp + ts, (long)(ng > 0 ? ng : 1) * 64) * (h_q / h_kv);
+  if (c > walk / 16) c = walk / 16;
   return (int)(c < 1 ? 1 : (c > 8 ? 8 : c));
 }
 
+// Problems whose stacked query tiles x heads cannot fill the 256 CUs tile each member's
+// responses on their own (see response_tiles in the planner): their time is the longest
+// tile walk, not the total work.
+constexpr long kSplitBelow = 256;
+
 Layout make_layout(int ng, int ns, int tp, int ts, int h_q, int h_kv, int d, bool bwd) {
-  (void)ns;
   Layout L{};
-  L.kv_chunks = bwd ? kv_chunks_for(ng, tp, h_kv) : 1;
-  L.max_q = ceil_div_l(tp, pg::kFwdBM) + ceil_div_l(ts, pg::kFwdBM) + 2L * ng;
-  L.max_kv = bwd ? (ceil_div_l(tp, pg::kKvBN) + ng) * L.kv_chunks + ceil_div_l(ts, pg::kKvBN) + ng : 0;
+  L.kv_chunks = bwd ? kv_chunks_for(ng, tp, ts, h_q, h_kv) : 1;
+  L.split = (ceil_div_l(tp, pg::kFwdBM) + ceil_div_l(ts, pg::kFwdBM) + ng) * (long)h_q < kSplitBelow ? 1 : 0;
+  // bounds of the tile lists in either tiling (splitting adds at most one tile per member)
+  L.max_q = ceil_div_l(tp, pg::kFwdBM) + ceil_div_l(ts, pg::kFwdBM) + 2L * ng + ns;
+  L.max_kv = bwd ? (ceil_div_l(tp, pg::kKvBN) + ng) * L.kv_chunks + ceil_div_l(ts, pg::kKvBN) + ng + ns : 0;
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
   const size_t rows = (size_t)tp + (size_t)ts;  // sizes are non-negative ints: no overflow in 64 bits
@@ -232,16 +243,17 @@ int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p,
   auto* qt = (pg::TileDesc*)(ws + L.qtiles);
   int* qo = (int*)(ws + L.qorder);
   if (L.max_q <= pg::kPlanThreads && (!bwd || L.max_kv <= pg::kPlanThreads) && !plan_multi()) {
-    // every tile list fits one block: groups, tiles and ranks in one launch
+    // every tile list fits one block: groups, tiles, ranks and the per-row member starts in one launch
     hipLaunchKernelGGL(pg::plan_fused_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, cu_p, cu_s, gsz, c.ng, c.ns,
-                       c.tp, c.ts, pg::kFwdBM, pg::kKvBN, L.kv_chunks, L.max_q, bwd ? L.max_kv : 0x7fffffffL, hdr, gi,
-                       qoff, kvoff, qt, qo, bwd ? (pg::TileDesc*)(ws + L.kvtiles) : nullptr, (int*)(ws + L.kvorder));
+                       c.tp, c.ts, pg::kFwdBM, pg::kKvBN, L.kv_chunks, L.split, L.max_q,
+                       bwd ? L.max_kv : 0x7fffffffL, hdr, gi, qoff, kvoff, qt, qo,
+                       bwd ? (pg::TileDesc*)(ws + L.kvtiles) : nullptr, (int*)(ws + L.kvorder), (int*)(ws + L.seg));
   } else {
     launch_plan_tiles(c, L, ws, cu_p, cu_s, gsz, st, bwd);
-  }
-  if (c.ts > 0) {
-    hipLaunchKernelGGL(pg::seg_start_kernel, dim3((unsigned)ceil_div_l(c.ts, 256)), dim3(256), 0, st, cu_s, c.ns,
-                       c.ts, hdr, (int*)(ws + L.seg));
+    if (c.ts > 0) {
+      hipLaunchKernelGGL(pg::seg_start_kernel, dim3((unsigned)ceil_div_l(c.ts, 256)), dim3(256), 0, st, cu_s, c.ns,
+                         c.ts, hdr, (int*)(ws + L.seg));
+    }
   }
   if (bwd && xl && c.tp + c.ts > 0) {
     hipLaunchKernelGGL(pg::xrow_kernel, dim3((unsigned)ceil_div_l((long)c.tp + c.ts, 256)), dim3(256), 0, st, cu_p,
@@ -258,14 +270,14 @@ void launch_plan_tiles(const Common& c, const Layout& L, char* ws, const int32_t
   int* qoff = (int*)(ws + L.qoff);
   int* kvoff = (int*)(ws + L.kvoff);
   hipLaunchKernelGGL(pg::plan_groups_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, cu_p, cu_s, gsz, c.ng, c.ns,
-                     c.tp, c.ts, pg::kFwdBM, pg::kKvBN, L.kv_chunks, L.max_q, bwd ? L.max_kv : 0x7fffffffL, hdr, gi, qoff,
-                     kvoff);
+                     c.tp, c.ts, pg::kFwdBM, pg::kKvBN, L.kv_chunks, L.split, L.max_q, bwd ? L.max_kv : 0x7fffffffL,
+                     hdr, gi, qoff, kvoff);
   auto* qt = (pg::TileDesc*)(ws + L.qtiles);
   int* qo = (int*)(ws + L.qorder);
   if (L.max_q > 0) {
     const int blocks = (int)ceil_div_l(L.max_q, 256);
     hipLaunchKernelGGL(pg::plan_tiles_kernel, dim3(blocks), dim3(256), 0, st, cu_s, c.ng, pg::kFwdBM, pg::kKvBN,
-                       1, (int)L.max_q, hdr, gi, qoff, qt, 0);
+                       1, L.split, (int)L.max_q, hdr, gi, qoff, qt, 0);
     hipLaunchKernelGGL(pg::plan_rank_kernel, dim3(blocks), dim3(256), 0, st, hdr, qt, qo, 0);
   }
   if (bwd && L.max_kv > 0) {
@@ -273,7 +285,7 @@ void launch_plan_tiles(const Common& c, const Layout& L, char* ws, const int32_t
     int* ko = (int*)(ws + L.kvorder);
     const int blocks = (int)ceil_div_l(L.max_kv, 256);
     hipLaunchKernelGGL(pg::plan_tiles_kernel, dim3(blocks), dim3(256), 0, st, cu_s, c.ng, pg::kFwdBM, pg::kKvBN,
-                       L.kv_chunks, (int)L.max_kv, hdr, gi, kvoff, kt, 1);
+                       L.kv_chunks, L.split, (int)L.max_kv, hdr, gi, kvoff, kt, 1);
     hipLaunchKernelGGL(pg::plan_rank_kernel, dim3(blocks), dim3(256), 0, st, hdr, kt, ko, 1);
   }
 }
@@ -454,8 +466,8 @@ int launch_rope_plan(const RopeLayout& L, char* ws, int ng, int ns, int tp, int 
                      const int32_t* cu_s, const int32_t* gsz, hipStream_t st) {
   auto* hdr = (pg::PlanHeader*)(ws + L.hdr);
   hipLaunchKernelGGL(pg::plan_groups_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, cu_p, cu_s, gsz, ng, ns, tp,
-                     ts, pg::kFwdBM, pg::kKvBN, 1, 0x7fffffffL, 0x7fffffffL, hdr, (pg::GroupInfoEx*)(ws + L.ginfo),
-                     (int*)(ws + L.qoff), (int*)(ws + L.kvoff));
+                     ts, pg::kFwdBM, pg::kKvBN, 1, 0, 0x7fffffffL, 0x7fffffffL, hdr,
+                     (pg::GroupInfoEx*)(ws + L.ginfo), (int*)(ws + L.qoff), (int*)(ws + L.kvoff));
   return finish_plan(hdr, st);
 }
 

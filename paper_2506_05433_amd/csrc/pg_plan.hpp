@@ -26,6 +26,8 @@ struct GroupInfoEx {
   int p0, p1, s0, s1, m0, m1, pad0, pad1;
 };
 
+__device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
 // Inclusive scan of one value per thread over a block of NT threads.
 template <int NT, typename V>
 __device__ __forceinline__ V block_inclusive_scan(V v, V* tmp) {
@@ -42,8 +44,6 @@ __device__ __forceinline__ V block_inclusive_scan(V v, V* tmp) {
   __syncthreads();
   return r;
 }
-
-__device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // Largest index i in [lo, hi) with a[i] <= x (a nondecreasing, a[lo] <= x).
 __device__ __forceinline__ int upper_index(const int* a, int lo, int hi, int x) {
@@ -65,11 +65,22 @@ struct PlanShared {
   int carry[3];
 };
 
+// Response tiles of a group: its response rows stacked into b-row tiles across member
+// boundaries, or (split) each member's rows tiled on their own. Stacking wastes no rows
+// and lets every tile share the group's prefix; splitting gives more, shorter tiles, which
+// is what a problem too small to fill the GPU needs (its time is the longest tile walk).
+__device__ inline int response_tiles(const int* __restrict__ cu_s, const GroupInfoEx& gi, int b, int split) {
+  if (!split) return ceil_div(gi.s1 - gi.s0, b);
+  int n = 0;
+  for (int m = gi.m0; m < gi.m1; ++m) n += ceil_div(cu_s[m + 1] - cu_s[m], b);
+  return n;
+}
+
 // One block of kPlanThreads threads. Validates and computes per-group ranges and tile offsets.
 __device__ inline void plan_groups_body(const int* __restrict__ cu_p, const int* __restrict__ cu_s,
                                         const int* __restrict__ gsz, int ng, int ns, int tp, int ts, int bm, int bkv,
-                                        int kv_chunks, long max_q, long max_kv, PlanHeader* hdr, GroupInfoEx* ginfo,
-                                        int* qoff, int* kvoff, PlanShared& sh) {
+                                        int kv_chunks, int split, long max_q, long max_kv, PlanHeader* hdr,
+                                        GroupInfoEx* ginfo, int* qoff, int* kvoff, PlanShared& sh) {
   int* tmp = sh.tmp;
   int& err = sh.err;
   int* carry = sh.carry;
@@ -117,8 +128,8 @@ __device__ inline void plan_groups_body(const int* __restrict__ cu_p, const int*
       gi.s0 = cu_s[gi.m0]; gi.s1 = cu_s[gi.m1];
       gi.pad0 = gi.pad1 = 0;
       ginfo[g] = gi;
-      nq = ceil_div(gi.p1 - gi.p0, bm) + ceil_div(gi.s1 - gi.s0, bm);
-      nkv = ceil_div(gi.p1 - gi.p0, bkv) * kv_chunks + ceil_div(gi.s1 - gi.s0, bkv);
+      nq = ceil_div(gi.p1 - gi.p0, bm) + response_tiles(cu_s, gi, bm, split);
+      nkv = ceil_div(gi.p1 - gi.p0, bkv) * kv_chunks + response_tiles(cu_s, gi, bkv, split);
     }
     const int iq = block_inclusive_scan<kPlanThreads>(nq, tmp);
     const int ikv = block_inclusive_scan<kPlanThreads>(nkv, tmp);
@@ -143,17 +154,18 @@ __device__ inline void plan_groups_body(const int* __restrict__ cu_p, const int*
 
 __global__ void __launch_bounds__(kPlanThreads) plan_groups_kernel(
     const int* __restrict__ cu_p, const int* __restrict__ cu_s, const int* __restrict__ gsz,
-    int ng, int ns, int tp, int ts, int bm, int bkv, int kv_chunks, long max_q, long max_kv,
+    int ng, int ns, int tp, int ts, int bm, int bkv, int kv_chunks, int split, long max_q, long max_kv,
     PlanHeader* hdr, GroupInfoEx* ginfo, int* qoff, int* kvoff) {
   __shared__ PlanShared sh;
-  plan_groups_body(cu_p, cu_s, gsz, ng, ns, tp, ts, bm, bkv, kv_chunks, max_q, max_kv, hdr, ginfo, qoff, kvoff, sh);
+  plan_groups_body(cu_p, cu_s, gsz, ng, ns, tp, ts, bm, bkv, kv_chunks, split, max_q, max_kv, hdr, ginfo, qoff, kvoff,
+                   sh);
 }
 
 // Descriptor of tile i (< the number of tiles). `which` 0 = query tiles, 1 = kv tiles.
 // Returns the tile's work (the ranking key).
 __device__ inline int plan_tile(int i, const int* __restrict__ cu_s, int ng, int bm, int bkv, int kv_chunks,
-                                 const GroupInfoEx* __restrict__ ginfo, const int* __restrict__ off, TileDesc* tiles,
-                                 int which) {
+                                 int split, const GroupInfoEx* __restrict__ ginfo, const int* __restrict__ off,
+                                 TileDesc* tiles, int which) {
   const int g = upper_index(off, 0, ng, i);  // off[ng] == n > i, groups with no tile share offsets
   // skip groups with zero tiles that share the offset of the next one
   const GroupInfoEx gi = ginfo[g];
@@ -181,8 +193,21 @@ __device__ inline int plan_tile(int i, const int* __restrict__ cu_s, int ng, int
     }
   } else {
     d.kind = 1;
-    d.row0 = gi.s0 + (local - np) * b;
-    d.row1 = min(d.row0 + b, gi.s1);
+    int lo = gi.s0, hi = gi.s1;  // the rows the tile is cut from: the group's, or one member's
+    local -= np;
+    if (split) {
+      for (int m = gi.m0; m < gi.m1; ++m) {
+        const int t = ceil_div(cu_s[m + 1] - cu_s[m], b);
+        if (local < t) {
+          lo = cu_s[m];
+          hi = cu_s[m + 1];
+          break;
+        }
+        local -= t;
+      }
+    }
+    d.row0 = lo + local * b;
+    d.row1 = min(d.row0 + b, hi);
     if (!which) {
       const int m = upper_index(cu_s, gi.m0, gi.m1, d.row0);
       d.aux = cu_s[m];                                  // first response key of the tile
@@ -198,13 +223,13 @@ __device__ inline int plan_tile(int i, const int* __restrict__ cu_s, int ng, int
 }
 
 // One thread per (possible) tile: fills the descriptors.
-__global__ void plan_tiles_kernel(const int* __restrict__ cu_s, int ng, int bm, int bkv, int kv_chunks, int max_tiles,
-                                  const PlanHeader* hdr, const GroupInfoEx* __restrict__ ginfo,
+__global__ void plan_tiles_kernel(const int* __restrict__ cu_s, int ng, int bm, int bkv, int kv_chunks, int split,
+                                  int max_tiles, const PlanHeader* hdr, const GroupInfoEx* __restrict__ ginfo,
                                   const int* __restrict__ off, TileDesc* tiles, int which) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   const int n = which ? hdr->n_kvtiles : hdr->n_qtiles;
   if (i >= n || i >= max_tiles) return;
-  plan_tile(i, cu_s, ng, bm, bkv, kv_chunks, ginfo, off, tiles, which);
+  plan_tile(i, cu_s, ng, bm, bkv, kv_chunks, split, ginfo, off, tiles, which);
 }
 
 // Longest-first order: order[rank] = tile, rank by (work desc, index asc). Deterministic.
@@ -275,17 +300,21 @@ __global__ void xrow_kernel(const int* __restrict__ cu_p, const int* __restrict_
 // block would walk every row.
 __global__ void __launch_bounds__(kPlanThreads) plan_fused_kernel(
     const int* __restrict__ cu_p, const int* __restrict__ cu_s, const int* __restrict__ gsz, int ng, int ns, int tp,
-    int ts, int bm, int bkv, int kv_chunks, long max_q, long max_kv, PlanHeader* hdr, GroupInfoEx* ginfo, int* qoff,
-    int* kvoff, TileDesc* qtiles, int* qorder, TileDesc* kvtiles, int* kvorder) {
+    int ts, int bm, int bkv, int kv_chunks, int split, long max_q, long max_kv, PlanHeader* hdr, GroupInfoEx* ginfo,
+    int* qoff, int* kvoff, TileDesc* qtiles, int* qorder, TileDesc* kvtiles, int* kvorder, int* seg_start) {
   __shared__ PlanShared sh;
-  plan_groups_body(cu_p, cu_s, gsz, ng, ns, tp, ts, bm, bkv, kv_chunks, max_q, max_kv, hdr, ginfo, qoff, kvoff, sh);
+  plan_groups_body(cu_p, cu_s, gsz, ng, ns, tp, ts, bm, bkv, kv_chunks, split, max_q, max_kv, hdr, ginfo, qoff, kvoff,
+                   sh);
   __syncthreads();
   const int t = threadIdx.x;
   // the tile counts the header now holds, taken from shared memory (both <= kPlanThreads, a host bound)
   const bool ok = !sh.err;
   const int nq = ok ? sh.carry[1] : 0, nkv = (kvtiles && ok) ? sh.carry[2] : 0;
-  const int wq = t < nq ? plan_tile(t, cu_s, ng, bm, bkv, 1, ginfo, qoff, qtiles, 0) : -1;
-  const int wkv = t < nkv ? plan_tile(t, cu_s, ng, bm, bkv, kv_chunks, ginfo, kvoff, kvtiles, 1) : -1;
+  const int wq = t < nq ? plan_tile(t, cu_s, ng, bm, bkv, 1, split, ginfo, qoff, qtiles, 0) : -1;
+  const int wkv = t < nkv ? plan_tile(t, cu_s, ng, bm, bkv, kv_chunks, split, ginfo, kvoff, kvtiles, 1) : -1;
+  // the per-row member starts (what seg_start_kernel computes), when asked for
+  if (seg_start && ok)
+    for (int r = t; r < ts; r += kPlanThreads) seg_start[r] = cu_s[upper_index(cu_s, 0, ns, r)];
   // longest-first ranks, the rule of plan_rank_kernel: (work desc, index asc)
   for (int which = 0; which < 2; ++which) {
     const int n = which ? nkv : nq;

@@ -41,20 +41,33 @@ def planner(tmp_path_factory):
     return exe
 
 
-def kv_chunks_for(ng, tp, h_kv):
+def kv_chunks_for(ng, tp, ts, h_q, h_kv):
     """The library's split of long prefix key walks (pg_attn.hip, kv_chunks_for)."""
     if tp <= 0 or h_kv <= 0:
         return 1
     tiles = (math.ceil(tp / BKV) + ng) * h_kv
-    return max(1, min(8, math.ceil(512 / tiles)))
+    c = math.ceil(512 / tiles)
+    walk = math.ceil((tp + ts) / (max(ng, 1) * 64)) * (h_q // h_kv)
+    c = min(c, walk // 16)
+    return max(1, min(8, c))
 
 
-def run_plan(exe, cu_p, cu_s, gsz, ng, ns, tp, ts, mode=0, kvc=1, max_q=None, max_kv=None):
-    if max_q is None:
-        max_q = math.ceil(tp / BM) + math.ceil(ts / BM) + 2 * ng
-    if max_kv is None:
-        max_kv = (math.ceil(tp / BKV) + ng) * kvc + math.ceil(ts / BKV) + ng
-    text = " ".join(str(int(x)) for x in [mode, ng, ns, tp, ts, BM, BKV, kvc, max_q, max_kv, *cu_p, *cu_s, *gsz])
+def split_for(ng, tp, ts, h_q):
+    """The library's choice of member-aligned response tiles (pg_attn.hip, make_layout)."""
+    return int((math.ceil(tp / BM) + math.ceil(ts / BM) + ng) * h_q < 256)
+
+
+def bounds(ng, ns, tp, ts, kvc):
+    return (math.ceil(tp / BM) + math.ceil(ts / BM) + 2 * ng + ns,
+            (math.ceil(tp / BKV) + ng) * kvc + math.ceil(ts / BKV) + ng + ns)
+
+
+def run_plan(exe, cu_p, cu_s, gsz, ng, ns, tp, ts, mode=0, kvc=1, split=0, max_q=None, max_kv=None):
+    bq, bkv = bounds(ng, ns, tp, ts, kvc)
+    max_q = bq if max_q is None else max_q
+    max_kv = bkv if max_kv is None else max_kv
+    text = " ".join(str(int(x)) for x in [mode, ng, ns, tp, ts, BM, BKV, kvc, split, max_q, max_kv, *cu_p, *cu_s,
+                                           *gsz])
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=0", UBSAN_OPTIONS="halt_on_error=1")
     res = subprocess.run([exe], input=text, capture_output=True, text=True, env=env, timeout=300)
     assert res.returncode == 0, res.stderr[-4000:]
@@ -113,25 +126,29 @@ def test_inconsistent_offsets_are_flagged(planner, bad):
         assert err == 1 and not q and not k
 
 
-def expected_tiles(prefix, groups, suffix, kvc):
-    """The tiling the kernels assume, as sets of (kind, group, row0, row1, aux, chunk, nchunks)."""
+def expected_tiles(prefix, groups, suffix, kvc, split=0):
+    """The tiling the kernels assume, as sets of (kind, group, row0, row1, aux, chunk, nchunks): prefix tiles
+    of every group; response rows of a group stacked into tiles across member boundaries, or with ``split``
+    each member's rows tiled on their own."""
     cu_p, cu_s, _ = arrays(prefix, groups, suffix)
     q, k = set(), set()
     m = 0
     for g, (p, gs) in enumerate(zip(prefix, groups)):
         p0, p1 = int(cu_p[g]), int(cu_p[g + 1])
-        s0, s1 = int(cu_s[m]), int(cu_s[m + gs])
+        spans = ([(int(cu_s[i]), int(cu_s[i + 1])) for i in range(m, m + gs)] if split
+                 else [(int(cu_s[m]), int(cu_s[m + gs]))])
         owner = lambda row: int(np.searchsorted(cu_s, row, side="right") - 1)  # noqa: E731
         for r0 in range(p0, p1, BM):
             q.add((0, g, r0, min(r0 + BM, p1), 0, 0, 1))
-        for r0 in range(s0, s1, BM):
-            q.add((1, g, r0, min(r0 + BM, s1), int(cu_s[owner(r0)]), 0, 1))
         for r0 in range(p0, p1, BKV):
             for c in range(kvc):
                 k.add((0, g, r0, min(r0 + BKV, p1), 0, c, kvc))
-        for r0 in range(s0, s1, BKV):
-            r1 = min(r0 + BKV, s1)
-            k.add((1, g, r0, r1, int(cu_s[owner(r1 - 1) + 1]), 0, 1))
+        for s0, s1 in spans:
+            for r0 in range(s0, s1, BM):
+                q.add((1, g, r0, min(r0 + BM, s1), int(cu_s[owner(r0)]), 0, 1))
+            for r0 in range(s0, s1, BKV):
+                r1 = min(r0 + BKV, s1)
+                k.add((1, g, r0, r1, int(cu_s[owner(r1 - 1) + 1]), 0, 1))
         m += gs
     return q, k
 
@@ -175,34 +192,35 @@ def check_loads(prefix, groups, suffix, q, k, seg, h_q, h_kv, d, dtype):
                 assert valid * h_q * d * el < 2 ** 31
 
 
-def _planned(planner, prefix, groups, suffix, h_kv, modes=(0, 1)):
+def _planned(planner, prefix, groups, suffix, h_q, h_kv, modes=(0, 1), split=None):
     """Plans of the one-block planner (only where the library uses it: both tile lists within one block)
-    and of the multi-kernel planner; modes=None: the planner the library would run."""
+    and of the multi-kernel planner; modes=None: the planner the library would run. ``split`` defaults to
+    the library's choice."""
     cu_p, cu_s, gsz = arrays(prefix, groups, suffix)
     ng, ns, tp, ts = len(prefix), len(suffix), int(cu_p[-1]), int(cu_s[-1])
-    kvc = kv_chunks_for(ng, tp, h_kv)
-    max_q = math.ceil(tp / BM) + math.ceil(ts / BM) + 2 * ng
-    max_kv = (math.ceil(tp / BKV) + ng) * kvc + math.ceil(ts / BKV) + ng
+    kvc = kv_chunks_for(ng, tp, ts, h_q, h_kv)
+    split = split_for(ng, tp, ts, h_q) if split is None else split
+    max_q, max_kv = bounds(ng, ns, tp, ts, kvc)
     one_block = max_q <= 1024 and max_kv <= 1024
     if modes is None:
         modes = (0,) if one_block else (1,)
-    plans = [run_plan(planner, cu_p, cu_s, gsz, ng, ns, tp, ts, mode=mode, kvc=kvc)
+    plans = [run_plan(planner, cu_p, cu_s, gsz, ng, ns, tp, ts, mode=mode, kvc=kvc, split=split)
              for mode in modes if mode == 1 or one_block]
-    return plans, kvc
+    return plans, kvc, split
 
 
-@pytest.mark.parametrize("seed", range(6))
-def test_random_groupings_plan_as_the_kernels_assume(planner, seed):
+@pytest.mark.parametrize("seed,split", [(s, s % 2) for s in range(6)])
+def test_random_groupings_plan_as_the_kernels_assume(planner, seed, split):
     rng = np.random.default_rng(seed)
     ng = int(rng.integers(1, 40))
     prefix = rng.integers(0, 600, ng) * (rng.random(ng) < 0.8)
     groups = rng.integers(0, 6, ng)
     suffix = rng.integers(0, 400, int(groups.sum())) * (rng.random(int(groups.sum())) < 0.9)
-    (fused, multi), kvc = _planned(planner, prefix, groups, suffix, h_kv=2)
+    (fused, multi), kvc, _ = _planned(planner, prefix, groups, suffix, 8, 2, split=split)
     assert fused == multi
     err, q, k, seg = fused
     assert err == 0
-    eq, ek = expected_tiles(list(prefix), list(groups), list(suffix), kvc)
+    eq, ek = expected_tiles(list(prefix), list(groups), list(suffix), kvc, split)
     assert set(t[:5] + t[6:] for t in q) == eq and len(q) == len(eq)
     assert set(t[:5] + t[6:] for t in k) == ek and len(k) == len(ek)
     for tiles in (q, k):
@@ -215,7 +233,7 @@ def test_random_groupings_plan_as_the_kernels_assume(planner, seed):
 def test_workload_loads_stay_in_range(planner, name):
     wl = WORKLOADS[name]
     prefix, groups, suffix = draw_lengths(wl, 0)
-    plans, _ = _planned(planner, prefix, groups, suffix, wl.h_kv)
+    plans, _, _ = _planned(planner, prefix, groups, suffix, wl.h_q, wl.h_kv)
     assert all(p == plans[0] for p in plans) and plans[0][0] == 0
     _, q, k, seg = plans[0]
     check_loads(prefix, groups, suffix, q, k, seg, wl.h_q, wl.h_kv, wl.head_dim, wl.dtype)
@@ -231,8 +249,8 @@ def test_fig23_grid_loads_stay_in_range(planner):
                 S = P // r
                 wl = Workload("grid", 1, G, ("fixed", P), ("uniform", S // 2, S + S // 2), 32, 8, 128, "bf16", 1.0)
                 prefix, groups, suffix = draw_lengths(wl, 0)
-                (plan,), _ = _planned(planner, prefix, groups, suffix, 8, modes=None)
+                (plan,), _, _ = _planned(planner, prefix, groups, suffix, 32, 8, modes=None)
                 check_loads(prefix, groups, suffix, plan[1], plan[2], plan[3], 32, 8, 128, "bf16")
     prefix, groups, suffix = [128], [16], [1024] * 16
-    (plan,), _ = _planned(planner, prefix, groups, suffix, 64, modes=None)
+    (plan,), _, _ = _planned(planner, prefix, groups, suffix, 512, 64, modes=None)
     check_loads(prefix, groups, suffix, plan[1], plan[2], plan[3], 512, 64, 128, "bf16")
