@@ -186,13 +186,15 @@ def shape_of(prob):
             prob.h_kv, prob.head_dim)
 
 
-def baseline_layout(torch, dev, prob, padded):
+def baseline_layout(torch, dev, prob, padded, copy=False):
     """The repeated-prefix layout (Eq. (1) without padding), or with ``padded`` the padded one (every member's
     response padded with zero rows to the group's longest), built on the device from the grouped tensors.
 
     Every member becomes a group of size 1 holding its own copy of the group's prefix; ``do_pre`` goes whole
     to a group's first copy and zero to the others, so the copies' summed prefix gradients equal the grouped
-    ones. Groups with no members keep their prefix as a group of size 0. Returns (device dict, shape)."""
+    ones. Groups with no members keep their prefix as a group of size 0. The unpadded layout shares the
+    response tensors with ``dev`` unless ``copy`` (so that a memory measurement counts them). Returns (device
+    dict, shape)."""
     import numpy as np
     cu_p, cu_s = prob.cu_prefix, prob.cu_suffix
     pre_idx, zero_do, prefix, groups, suffix, suf_src = [], [], [], [], [], []
@@ -236,7 +238,7 @@ def baseline_layout(torch, dev, prob, padded):
             out[name] = t
     else:
         for name in ("q_suf", "k_suf", "v_suf", "do_suf"):
-            out[name] = dev[name]
+            out[name] = dev[name].clone() if copy else dev[name]
     i32 = lambda a: torch.from_numpy(np.asarray(a, np.int32)).to(where)  # noqa: E731
     out["cu_prefix"] = i32(np.concatenate([[0], np.cumsum(prefix)]))
     out["cu_suffix"] = i32(np.concatenate([[0], np.cumsum(suffix)]))
@@ -482,19 +484,22 @@ def sweep(args):
                 for name in ("grouped", "repeated", "padded"):
                     # names the case before any GPU work on it
                     print(f"[sweep] P={P} G={G} r={r} {name}", flush=True)
+                    # the baselines are gathered from the grouped tensors, which are allocated before the
+                    # measured region; each layout's peak counts its own inputs, outputs, gradients and
+                    # workspaces
+                    src = binding.to_device(prob, "cuda") if name != "grouped" else None
 
                     def build():
-                        dev = binding.to_device(prob, "cuda")
-                        shape = shape_of(prob)
-                        if name != "grouped":
-                            bdev, shape = baseline_layout(torch, dev, prob, padded=name == "padded")
-                            del dev
-                            dev = bdev
+                        if name == "grouped":
+                            dev, shape = binding.to_device(prob, "cuda"), shape_of(prob)
+                        else:
+                            dev, shape = baseline_layout(torch, src, prob, padded=name == "padded", copy=True)
                         bufs = alloc(binding, torch, dev, shape)
                         step_fn(binding, dev, bufs)()
                         return dev, bufs
 
                     peak, (dev, bufs) = measured_peak_bytes(torch, build)
+                    del src
                     res = time_layout(binding, torch, dev, bufs, args.steps, args.warmup, flush, name, eager=False)
                     out[name + "_ms"] = round(statistics.median(res["graph_ms"]), 4)
                     out[name + "_peak_MB"] = round(peak / 1e6, 1)

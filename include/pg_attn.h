@@ -45,9 +45,10 @@
  * Errors: each call returns a pg_status. Host-side argument checks run before
  * anything is launched, and on error no output is touched. The consistency of
  * the device grouping arrays is checked on the device: if they are
- * inconsistent no attention work is done (outputs are left as they were) and,
- * only when the environment variable PG_DEBUG_VALIDATE=1 is set (which makes
- * the call synchronise), PG_EINVAL is returned. HIP failures return PG_EHIP.
+ * inconsistent no attention work is done (outputs are left as they were);
+ * pg_plan_status() reports that afterwards, and with the environment variable
+ * PG_DEBUG_VALIDATE=1 (which makes every call synchronise) the call itself
+ * returns PG_EINVAL. HIP failures return PG_EHIP.
  * pg_last_error() gives a message for the calling thread's last failure.
  *
  * Planning: each attention call first plans its tiles on the device, in one
@@ -264,6 +265,17 @@ typedef enum {
 int pg_timing_start(void);
 int pg_timing_stop(void);
 int pg_timing_get(int kernel, int* launches, double* total_ms);
+
+/*
+ * Verdict of the device-side check of the grouping arrays in the last call
+ * that used this workspace (pg_attn_fwd, pg_attn_bwd, their _xours forms,
+ * pg_attn_fwd_last, pg_rope, pg_grouped_positions), or with workspace == NULL
+ * the last pg_attn_fwd_noalloc on the current device: PG_OK when they were
+ * consistent, PG_EINVAL when they were not (that call did no work). It waits
+ * for the stream (the one that call used) to finish. PG_EWORKSPACE when the
+ * workspace is smaller than a plan header (256 bytes).
+ */
+int pg_plan_status(const void* workspace, size_t workspace_bytes, void* stream);
 
 /* Static description of a status code. */
 const char* pg_status_string(int status);

@@ -37,6 +37,7 @@ SIGNATURES = {
     "pg_timing_start": (_I, []),
     "pg_timing_stop": (_I, []),
     "pg_timing_get": (_I, [_I, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)]),
+    "pg_plan_status": (_I, [_P, _Z, _P]),
     "pg_status_string": (ctypes.c_char_p, [_I]),
     "pg_last_error": (ctypes.c_char_p, []),
 }
@@ -206,6 +207,17 @@ def bwd(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, o_pre, o_suf, lse_pre, lse_suf
         _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(torch, dev))
     _check(st)
     return out
+
+
+def plan_status(workspace=None):
+    """Raise PgError(PG_EINVAL) if the last call that used ``workspace`` (None: the last pg_attn_fwd_noalloc on
+    the current device) found its grouping arrays inconsistent; waits for the current stream."""
+    import torch
+    if workspace is None:
+        st = lib().pg_plan_status(None, 0, _stream(torch, torch.device("cuda", torch.cuda.current_device())))
+    else:
+        st = lib().pg_plan_status(_ptr(workspace), workspace.numel(), _stream(torch, workspace.device))
+    _check(st)
 
 
 def fwd_noalloc(q_pre, k_pre, v_pre, q_suf, k_suf, v_suf, cu_prefix, cu_suffix, group_sizes, scale, out):

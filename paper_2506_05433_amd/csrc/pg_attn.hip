@@ -506,6 +506,25 @@ const char* pg_status_string(int s) {
 
 const char* pg_last_error(void) { return g_last_error.c_str(); }
 
+int pg_plan_status(const void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  const void* hdr = workspace;
+  if (!workspace) {
+    void* p = nullptr;
+    const int rc = scratch_ptr(&p);
+    if (rc) return rc;
+    hdr = p;  // every planned call puts the plan header at offset 0
+  } else if (workspace_bytes < sizeof(pg::PlanHeader)) {
+    return fail(PG_EWORKSPACE, "workspace of %zu bytes cannot hold a plan header", workspace_bytes);
+  }
+  int err = 0;
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = hipMemcpyAsync(&err, hdr, sizeof(int), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "plan status readback");
+  return err ? fail(PG_EINVAL, "grouping arrays are inconsistent (checked on the device)") : PG_OK;
+}
+
 int pg_attn_fwd(int dtype, int n_groups, int n_suffixes, int total_prefix, int total_suffix,
                 const int32_t* cu_prefix_lens, const int32_t* cu_suffix_lens, const int32_t* group_sizes,
                 int h_q, int h_kv, int head_dim, float softmax_scale,

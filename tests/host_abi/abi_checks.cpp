@@ -107,6 +107,7 @@ int main() {
     ++g_bad;
   }
   if (pg_rope_workspace_size(0x7fffffff) == 0) { printf("MISMATCH rope size\n"); ++g_bad; }
+  expect("plan status small workspace", pg_plan_status(p, 16, nullptr), PG_EWORKSPACE);
   // status strings and timing queries
   for (int s = -1; s <= 5; ++s)
     if (!pg_status_string(s) || !*pg_status_string(s)) { printf("MISMATCH status string %d\n", s); ++g_bad; }

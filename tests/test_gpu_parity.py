@@ -302,6 +302,18 @@ def test_invalid_grouping_arrays_do_no_work(monkeypatch):
                 dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], dev["scale"], out=(o_pre, o_suf, lp, ls))
     torch.cuda.synchronize()
     assert bool((o_pre == 7.0).all()) and bool((o_suf == 7.0).all())
+    # the device's verdict, read back from the call's workspace on request
+    ws = torch.empty(binding.workspace_bytes("fwd", 1, 2, 64, 30, 2, 1, 64), device="cuda", dtype=torch.uint8)
+    binding.fwd(dev["q_pre"], dev["k_pre"], dev["v_pre"], dev["q_suf"], dev["k_suf"], dev["v_suf"],
+                dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], dev["scale"], out=(o_pre, o_suf, lp, ls),
+                workspace=ws)
+    with pytest.raises(binding.PgError) as e:
+        binding.plan_status(ws)
+    assert e.value.status == 1
+    good = binding.to_device(prob, "cuda")
+    binding.fwd(good["q_pre"], good["k_pre"], good["v_pre"], good["q_suf"], good["k_suf"], good["v_suf"],
+                good["cu_prefix"], good["cu_suffix"], good["group_sizes"], good["scale"], workspace=ws)
+    binding.plan_status(ws)
     monkeypatch.setenv("PG_DEBUG_VALIDATE", "1")
     with pytest.raises(binding.PgError) as e:
         binding.fwd(dev["q_pre"], dev["k_pre"], dev["v_pre"], dev["q_suf"], dev["k_suf"], dev["v_suf"],

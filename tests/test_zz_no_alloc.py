@@ -46,3 +46,25 @@ def test_noalloc_forward_equals_workspace_forward_twice_shrinking():
                        grads=False)
     for name, g in zip(OUTS, got):
         check(name, g, o[name], small.dtype)
+
+
+def test_noalloc_plan_status_reports_inconsistent_grouping():
+    """With inconsistent grouping arrays the allocation-free forward does no work, and pg_plan_status reads
+    that verdict from the scratch array; a consistent call after it clears it."""
+    from paper_2506_05433_amd import binding
+    prob = make_problem("single_group", seed=23, lengths=((64,), (2,), (10, 20)), h_q=2, h_kv=1, head_dim=64)
+    dev = binding.to_device(prob, "cuda")
+    out = _outputs_like(dev, prob)
+    bad = torch.tensor([0, 25, 20], dtype=torch.int32, device="cuda")  # not nondecreasing
+    args = (dev["q_pre"], dev["k_pre"], dev["v_pre"], dev["q_suf"], dev["k_suf"], dev["v_suf"], dev["cu_prefix"])
+    binding.fwd_noalloc(*args, bad, dev["group_sizes"], dev["scale"], out=out)
+    with pytest.raises(binding.PgError) as e:
+        binding.plan_status()
+    assert e.value.status == 1
+    assert bool((out[0] == 3.0).all()) and bool((out[1] == 3.0).all())
+    binding.fwd_noalloc(*args, dev["cu_suffix"], dev["group_sizes"], dev["scale"], out=out)
+    binding.plan_status()
+    ref = binding.run_fwd(dev)
+    torch.cuda.synchronize()
+    for g, r in zip(out, ref):
+        assert torch.equal(g, r)
