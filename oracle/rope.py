@@ -10,8 +10,8 @@ prefix row t of a group sits at position t and row j of any member's response
 sits at position P + j. Algorithm 1 takes q and k already rotary-encoded;
 this module is that step.
 
-The rotary embedding itself is not defined in the paper ("RoPE or its
-variants"). The standard definition is followed: the first ``rotary_dim``
+The paper names rotary embeddings without defining them. The standard
+definition is followed: the first ``rotary_dim``
 dimensions of a head vector form rotary_dim / 2 pairs; pair i is rotated by
 the angle pos * base ** (-2 i / rotary_dim); the remaining dimensions pass
 through unchanged. Two pair layouts are in use and both are provided:
