@@ -232,6 +232,8 @@ int finish_plan(const pg::PlanHeader* hdr, hipStream_t st) {
 void launch_plan_tiles(const Common& c, const Layout& L, char* ws, const int32_t* cu_p, const int32_t* cu_s,
                        const int32_t* gsz, hipStream_t st, bool bwd);
 
+constexpr int kFusedSegRows = 8192;
+
 // Runs the planner kernels. `bwd` also builds the key/value tile list.
 int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p, const int32_t* cu_s,
                 const int32_t* gsz, hipStream_t st, bool bwd, bool xl) {
@@ -242,18 +244,23 @@ int launch_plan(const Common& c, const Layout& L, char* ws, const int32_t* cu_p,
   int* kvoff = (int*)(ws + L.kvoff);
   auto* qt = (pg::TileDesc*)(ws + L.qtiles);
   int* qo = (int*)(ws + L.qorder);
-  if (L.max_q <= pg::kPlanThreads && (!bwd || L.max_kv <= pg::kPlanThreads) && !plan_multi()) {
-    // every tile list fits one block: groups, tiles, ranks and the per-row member starts in one launch
+  // the one-block planner also fills the per-row member starts when there are few rows (one
+  // launch less; over many rows one block is slower than the wide kernel)
+  const bool one_block = L.max_q <= pg::kPlanThreads && (!bwd || L.max_kv <= pg::kPlanThreads) && !plan_multi();
+  const bool fused_seg = one_block && c.ts <= kFusedSegRows;
+  if (one_block) {
+    // every tile list fits one block: groups, tiles and ranks in one launch
     hipLaunchKernelGGL(pg::plan_fused_kernel, dim3(1), dim3(pg::kPlanThreads), 0, st, cu_p, cu_s, gsz, c.ng, c.ns,
                        c.tp, c.ts, pg::kFwdBM, pg::kKvBN, L.kv_chunks, L.split, L.max_q,
                        bwd ? L.max_kv : 0x7fffffffL, hdr, gi, qoff, kvoff, qt, qo,
-                       bwd ? (pg::TileDesc*)(ws + L.kvtiles) : nullptr, (int*)(ws + L.kvorder), (int*)(ws + L.seg));
+                       bwd ? (pg::TileDesc*)(ws + L.kvtiles) : nullptr, (int*)(ws + L.kvorder),
+                       fused_seg ? (int*)(ws + L.seg) : nullptr);
   } else {
     launch_plan_tiles(c, L, ws, cu_p, cu_s, gsz, st, bwd);
-    if (c.ts > 0) {
-      hipLaunchKernelGGL(pg::seg_start_kernel, dim3((unsigned)ceil_div_l(c.ts, 256)), dim3(256), 0, st, cu_s, c.ns,
-                         c.ts, hdr, (int*)(ws + L.seg));
-    }
+  }
+  if (c.ts > 0 && !fused_seg) {
+    hipLaunchKernelGGL(pg::seg_start_kernel, dim3((unsigned)ceil_div_l(c.ts, 256)), dim3(256), 0, st, cu_s, c.ns,
+                       c.ts, hdr, (int*)(ws + L.seg));
   }
   if (bwd && xl && c.tp + c.ts > 0) {
     hipLaunchKernelGGL(pg::xrow_kernel, dim3((unsigned)ceil_div_l((long)c.tp + c.ts, 256)), dim3(256), 0, st, cu_p,
