@@ -56,15 +56,17 @@ struct Layout {
 // two per CU), at most 8, and 1 when there are already that many prefix key tiles. More
 // pieces balance better but each adds a full fp32 partial to write and reduce; measured on
 // the single-group and large-group workloads, 512 beats 256 and 1024-4096. A piece keeps at
-// least 16 query tiles of the average walk (a group's rows, once per query head of the kv
-// head): shorter pieces cost more in their fixed start-up and in the reduce launch than they
-// save.
+// least 16 64-row query tiles of the average walk (a group's rows, once per query head of
+// the kv head): shorter pieces cost more in their fixed start-up and in the reduce launch
+// than they save. A grid of at most 128 key tiles (half the CUs) runs as long as its
+// longest walk whatever the total work, so there pieces of one such tile pay off.
 int kv_chunks_for(int ng, int tp, int ts, int h_q, int h_kv) {
   if (tp <= 0 || h_kv <= 0) return 1;
   const long tiles = (ceil_div_l(tp, pg::kKvBN) + ng) * (long)h_kv;
   long c = ceil_div_l(512, tiles);
   const long walk = ceil_div_l((long)tp + ts, (long)(ng > 0 ? ng : 1) * 64) * (h_q / h_kv);
-  if (c > walk / 16) c = walk / 16;
+  const long min_piece = 2 * tiles <= 256 ? 1 : 16;
+  if (c > walk / min_piece) c = walk / min_piece;
   return (int)(c < 1 ? 1 : (c > 8 ? 8 : c));
 }
 

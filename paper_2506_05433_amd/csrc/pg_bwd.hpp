@@ -45,7 +45,7 @@ struct BwdArgs {
 
 // ------------------------------------------------------------------ dK, dV (key-stationary)
 // A workgroup owns 128 keys of one kv head, split into four groups of 32. Each key
-// group is served by two waves that share a SIMD:
+// group is served by two waves (on one SIMD, or on two when the key tile is ragged):
 //   P-wave : S = Q K^T, P = exp(S*scale - lse) (masked), dV^T += dO^T P; it hands P
 //            (bf16 operand fragments) to its partner through LDS;
 //   G-wave : one query tile behind, dP = dO V^T, dS = P (dP - Dsum), dK^T += Q^T dS.
@@ -95,8 +95,13 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
 
   const int tid = threadIdx.x, wave = uniform(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hh = lane >> 5;
-  const int grp = wave % kKvGroups;
   const bool pwave = wave < kKvGroups;
+  // Key group of the wave. Waves run on SIMD wave % 4. With all four key groups holding keys,
+  // the P- and G-wave of a group share a SIMD; a ragged key tile (fewer groups) pairs the
+  // G-wave of group g with SIMD (g + 2) % 4 instead, so that its active waves spread over
+  // all four SIMDs.
+  const bool ragged = td.row1 - td.row0 <= kKvBN - 32;
+  const int grp = (pwave || !ragged) ? wave % kKvGroups : (wave + kKvGroups / 2) % kKvGroups;
   const int wk0 = td.row0 + 32 * grp;             // first key of this key group
   const bool wave_active = wk0 < td.row1;
   const int wk1 = min(wk0 + 32, td.row1) - 1;     // last valid key of the group
@@ -229,6 +234,9 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     }
   };
 
+  // The G-waves (one tile behind, the longer chain of each tile) issue first when both waves
+  // of a SIMD are ready.
+  if (!pwave) __builtin_amdgcn_s_setprio(1);
   if (pwave) {
     walk_tiles([&](int it, const TileInfo& ti, const TileInfo&) {
       if (!(it < it1 && wave_active)) return;

@@ -48,7 +48,7 @@ def kv_chunks_for(ng, tp, ts, h_q, h_kv):
     tiles = (math.ceil(tp / BKV) + ng) * h_kv
     c = math.ceil(512 / tiles)
     walk = math.ceil((tp + ts) / (max(ng, 1) * 64)) * (h_q // h_kv)
-    c = min(c, walk // 16)
+    c = min(c, walk // (1 if 2 * tiles <= 256 else 16))
     return max(1, min(8, c))
 
 
