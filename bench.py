@@ -181,6 +181,27 @@ def alloc(binding, torch, dev, prob_shape):
     return bufs
 
 
+def copy_sum_fn(torch, prob, bufs):
+    """The step a repeated-layout trainer adds after its backward to recover the shared prefix's gradients: the
+    G-way sum of each group's prefix copies of dQ, dK and dV (timed apart from the kernels, on the device)."""
+    segs, row = [], 0
+    for p, gs in zip(prob.prefix_lens, prob.group_sizes):
+        p, gs = int(p), int(gs)
+        if gs > 1 and p > 0:
+            segs.append((row, gs, p))
+        row += max(gs, 1) * p
+    grads = bufs["bwd"][:3]  # dq_pre, dk_pre, dv_pre of the repeated layout
+    outs = [[torch.empty((p,) + tuple(t.shape[1:]), device=t.device, dtype=t.dtype) for (_, _, p) in segs]
+            for t in grads]
+
+    def run():
+        for t, o in zip(grads, outs):
+            for (r0, gs, p), dst in zip(segs, o):
+                torch.sum(t[r0:r0 + gs * p].view(gs, p, *t.shape[1:]), dim=0, out=dst)
+    run.outs = outs  # [gradient][group with copies]
+    return run
+
+
 def shape_of(prob):
     return (len(prob.prefix_lens), len(prob.suffix_lens), prob.total_prefix, prob.total_suffix, prob.h_q,
             prob.h_kv, prob.head_dim)
@@ -383,7 +404,18 @@ def cpu_baseline(prob, budget_s):
             "sample": f"{len(units)} (group, query head) units [{desc}] of {ng} groups x {prob.h_q} heads "
                       f"(groups P={[int(prob.prefix_lens[g]) for g in sorted(set(u[0] for u in units))]}), "
                       f"all rows and members of each, fp64 numpy, repeated-prefix, fwd+bwd; {total_s:.1f} s",
-            "seconds": round(total_s, 2), "host_cpus": len(os.sched_getaffinity(0))}
+            "seconds": round(total_s, 2), "host_cpus": len(os.sched_getaffinity(0)), "cpu_model": cpu_model()}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 ATTN_SOURCES = ("pg_attn.hip", "pg_bwd.hpp", "pg_common.hpp", "pg_fwd.hpp", "pg_plan.hpp", "pg_types.hpp")
@@ -625,6 +657,14 @@ def main():
             progress(f"{name} layout: {rms:.3f} ms/step")
             out[f"{name}_ms_per_step"] = round(rms, 4)
             out[f"speedup_vs_{name}"] = round(rms / ms, 3)
+            if name == "repeated":
+                run = copy_sum_fn(torch, prob, bbufs)
+                for _ in range(max(args.warmup, 1)):
+                    run()
+                csum = statistics.median(timed_steps(torch, run, min(args.steps, 10), flush, "prefix copy sum"))
+                # reported apart: the kernels' speedup above does not include it
+                out["repeated_prefix_copy_sum_ms"] = round(csum, 4)
+                out["speedup_vs_repeated_with_copy_sum"] = round((rms + csum) / ms, 3)
             del bdev, bbufs
             torch.cuda.empty_cache()
         if args.padded:

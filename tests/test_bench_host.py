@@ -140,3 +140,29 @@ def test_cpu_baseline_units_are_the_oracle_on_one_group_and_head():
     assert np.array_equal(r["dq_suf"][:, 0], full["dq_suf"][4:15, 3])
     res = bench.cpu_baseline(prob, 1.0)
     assert res["kind"] == "oracle" and res["value"] > 0 and res["cores"] >= 1
+
+
+def test_prefix_copy_sum_adds_each_groups_copies():
+    """The repeated layout's separately timed extra step: the G-way sum of each group's prefix gradient copies,
+    checked against a loop over the copies (groups of size 0 and 1 have nothing to add)."""
+    from paper_2506_05433_amd.inputs import make_problem
+    import torch
+    prob = make_problem("single_group", seed=3, lengths=((5, 0, 7, 3), (2, 1, 0, 3), (4, 0, 6, 1, 2, 3)), h_q=4,
+                        h_kv=2, head_dim=64)
+    _, shape = bench.baseline_layout(torch, _cpu_dev(prob), prob, padded=False)
+    rows = shape[2]
+    g = torch.Generator().manual_seed(0)
+    grads = tuple(torch.randn((rows, h, 64), generator=g) for h in (4, 2, 2))
+    run = bench.copy_sum_fn(torch, prob, {"bwd": grads})
+    run()
+    # expected: walk the layout's prefix rows group by group
+    row, k = 0, 0
+    for p, gs in zip(prob.prefix_lens, prob.group_sizes):
+        p, gs = int(p), int(gs)
+        if gs > 1 and p > 0:
+            for t, outs in zip(grads, run.outs):
+                want = sum(t[row + i * p: row + (i + 1) * p] for i in range(gs))
+                assert torch.allclose(outs[k], want, atol=1e-5)
+            k += 1
+        row += max(gs, 1) * p
+    assert row == rows and k == len(run.outs[0]) == 2
