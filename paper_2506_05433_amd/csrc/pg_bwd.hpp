@@ -52,8 +52,8 @@ struct BwdArgs {
 // Each wave therefore holds one kv operand and one accumulator (about half the
 // registers of a wave doing all four products), so two waves fit per SIMD and one's
 // exp/VALU work overlaps the other's matrix instructions. Query tiles are
-// triple-buffered in LDS (P-waves read tile i, G-waves tile i-1, tile i+1 loads through
-// registers and is written to LDS after the work on tile i).
+// triple-buffered in LDS (P-waves read tile i, G-waves tile i-1; the G-waves load tile
+// i+1 through registers and write it to LDS after their work on tile i-1).
 constexpr int kKvGroups = 4;                 // 32-key groups per workgroup
 constexpr int kKvBN = 32 * kKvGroups;        // keys per workgroup
 constexpr int kKvThreads = 128 * kKvGroups;  // a P-wave and a G-wave per key group
@@ -170,26 +170,32 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     }
   };
 
-  // Query tiles are staged through registers (16 per thread), not copied straight into
-  // LDS: with the three buffers in one LDS array indexed at run time, a direct copy into
-  // one of them would make every read of another wait for the copy to land.
-  TileLoader<T, BQ, D, kKvThreads> ldq, ldo;
-  ldq.init(a.h_q * D, wave, lane);
-  ldo.init(a.h_q * D, wave, lane);
+  // Query tiles are staged through registers, not copied straight into LDS: with the three
+  // buffers in one LDS array indexed at run time, a direct copy into one of them would make
+  // every read of another wait for the copy to land. The G-waves stage them (and the per-row
+  // values below): with the G-waves issuing first, the P-waves are the longer chain of a
+  // tile, and the G-waves wait for them at the barrier.
+  TileLoader<T, BQ, D, kKvThreads / 2> ldq, ldo;
+  ldq.init(a.h_q * D, wave - kKvGroups, lane);  // used by the G-waves only
+  ldo.init(a.h_q * D, wave - kKvGroups, lane);
   FragOffsets<T, D> fo;
   fo.init(lane);
   // per-row values of the next tile: loaded with its copies, used only in commit() (a use
   // right after the load would wait for the copies issued before it as well)
   float pf_lse = 0.f, pf_dsum = 0.f;
   int pf_seg = 0;
+  const int rl = tid - 64 * kKvGroups;  // row of this lane of the first G-wave
+  const bool row_lane = rl >= 0 && rl < BQ;
   auto issue = [&](const TileInfo& ti, int it) {  // `it` selects the buffer
     const T* Qs = (const T*)(ti.qsuf ? a.q_suf : a.q_pre);
     const T* Gs = (const T*)(ti.qsuf ? a.do_suf : a.do_pre);
     const size_t off = ((size_t)(ti.q0 + (ti.qsuf ? xo_suf : xo_pre)) * a.h_q + ti.hq) * D;
-    ldq.load(smem[it % NBUF][0], Qs + off, a.h_q * D, ti.qend - ti.q0);
-    ldo.load(smem[it % NBUF][1], Gs + off, a.h_q * D, ti.qend - ti.q0);
-    if (tid < BQ) {
-      const int q = min(ti.q0 + tid, ti.qend - 1);  // padding rows read the last row; commit() drops them
+    if (!pwave) {
+      ldq.load(smem[it % NBUF][0], Qs + off, a.h_q * D, ti.qend - ti.q0);
+      ldo.load(smem[it % NBUF][1], Gs + off, a.h_q * D, ti.qend - ti.q0);
+    }
+    if (row_lane) {
+      const int q = min(ti.q0 + rl, ti.qend - 1);  // padding rows read the last row; commit() drops them
       const float* L = ti.qsuf ? a.lse_suf : a.lse_pre;
       const int ld = ti.qsuf ? lse_ld_suf : lse_ld_pre;
       pf_lse = L[(size_t)ti.hq * ld + q + (ti.qsuf ? xo_suf : xo_pre)];
@@ -198,13 +204,15 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     }
   };
   auto commit = [&](const TileInfo& ti, int buf) {
-    ldq.store(smem[buf][0]);
-    ldo.store(smem[buf][1]);
-    if (tid < BQ) {
-      const bool v = ti.q0 + tid < ti.qend;
-      s_lse[buf][tid] = v ? pf_lse * kLog2e : INFINITY;  // padding rows: P = 0
-      s_dsum[buf][tid] = v ? pf_dsum : 0.f;
-      s_seg[buf][tid] = (v && ti.qsuf) ? pf_seg : 0;
+    if (!pwave) {
+      ldq.store(smem[buf][0]);
+      ldo.store(smem[buf][1]);
+    }
+    if (row_lane) {
+      const bool v = ti.q0 + rl < ti.qend;
+      s_lse[buf][rl] = v ? pf_lse * kLog2e : INFINITY;  // padding rows: P = 0
+      s_dsum[buf][rl] = v ? pf_dsum : 0.f;
+      s_seg[buf][rl] = (v && ti.qsuf) ? pf_seg : 0;
     }
   };
 
