@@ -116,6 +116,10 @@ __global__ void __launch_bounds__(kKvThreads, 512 / kKvThreads) dkdv_kernel(cons
     const size_t off = ((size_t)(key_c + xk) * a.h_kv + kvh) * D + 8 * hh;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) kv[kk] = E::global_row(B + off + 16 * kk, kvalid);
+    // wait for them here, on every path: otherwise the compiler, unsure whether they landed,
+    // waits for all outstanding loads (the next tile's copies included) before the first
+    // product of every tile
+    __builtin_amdgcn_s_waitcnt(0);
   }
   f32x16 acc[DB];  // dV^T (P-wave) or dK^T (G-wave)
 #pragma unroll
