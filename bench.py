@@ -303,6 +303,49 @@ def time_last(binding, torch, dev, prob, steps, warmup):
             "peak_GBps": 8000.0, "frac": round(gbs / 8000.0, 4), "bound": "hbm", "queries": ns * prob.h_q}
 
 
+def time_xours(binding, torch, dev, prob, steps, warmup, flush, split_ms):
+    """The same fwd+bwd step through the single-buffer calls of Eq. (2) (pg_attn_fwd_xours / pg_attn_bwd_xours):
+    every tensor one buffer holding, group after group, the prefix rows and then the members' response rows.
+    Timed like the headline (median of cache-flushed HIP-graph replays); same kernels, so the ratio to the
+    split-buffer step should be ~1."""
+    import numpy as np
+    cu_p, cu_s, tp = prob.cu_prefix, prob.cu_suffix, prob.total_prefix
+    order, m = [], 0
+    for g, gs in enumerate(prob.group_sizes):
+        order.append(np.arange(cu_p[g], cu_p[g + 1]))
+        order.append(tp + np.arange(cu_s[m], cu_s[m + int(gs)]))
+        m += int(gs)
+    idx = torch.from_numpy(np.concatenate(order).astype(np.int64)).to(dev["q_pre"].device)
+    x = {n: torch.cat([dev[n + "_pre"], dev[n + "_suf"]]).index_select(0, idx) for n in ("q", "k", "v", "do")}
+    grp = (dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], tp, dev["scale"])
+    rows = x["q"].shape[0]
+    fo = (torch.empty_like(x["q"]), torch.empty((prob.h_q, rows), device="cuda", dtype=torch.float32))
+    bo = (torch.empty_like(x["q"]), torch.empty_like(x["k"]), torch.empty_like(x["v"]))
+    shape = shape_of(prob)
+    ws_f = torch.empty(binding.workspace_bytes("fwd", *shape), device="cuda", dtype=torch.uint8)
+    ws_b = torch.empty(binding.workspace_bytes("bwd", *shape), device="cuda", dtype=torch.uint8)
+
+    def step():
+        binding.fwd_xours(x["q"], x["k"], x["v"], *grp, out=fo, workspace=ws_f)
+        binding.bwd_xours(x["q"], x["k"], x["v"], fo[0], fo[1], x["do"], *grp, out=bo, workspace=ws_b)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    ms = statistics.median(timed_steps(torch, graph.replay, steps, flush, "single-buffer layout"))
+    del graph, x, fo, bo, ws_f, ws_b
+    torch.cuda.empty_cache()
+    return {"ms_per_step": round(ms, 4), "vs_split_layout": round(split_ms / ms, 3)}
+
+
 def time_rope(binding, torch, dev, prob, steps, warmup):
     """The grouped-position rotary embedding of q and k (both sides) on this workload, out of place.
 
@@ -642,6 +685,7 @@ def main():
     if not args.no_extras:
         out["rope"] = time_rope(binding, torch, dev, prob, args.steps, args.warmup)
         out["last"] = time_last(binding, torch, dev, prob, args.steps, args.warmup)
+        out["xours"] = time_xours(binding, torch, dev, prob, args.steps, args.warmup, flush, ms)
     if not args.no_repeated:
         out["speedup_ceiling_pairs"] = round(rep_pairs / pairs, 3)
         G, P, sum_s = prob.group_sizes, prob.prefix_lens, prob.suffix_lens.sum()
