@@ -308,14 +308,9 @@ def time_xours(binding, torch, dev, prob, steps, warmup, flush, split_ms):
     every tensor one buffer holding, group after group, the prefix rows and then the members' response rows.
     Timed like the headline (median of cache-flushed HIP-graph replays); same kernels, so the ratio to the
     split-buffer step should be ~1."""
-    import numpy as np
-    cu_p, cu_s, tp = prob.cu_prefix, prob.cu_suffix, prob.total_prefix
-    order, m = [], 0
-    for g, gs in enumerate(prob.group_sizes):
-        order.append(np.arange(cu_p[g], cu_p[g + 1]))
-        order.append(tp + np.arange(cu_s[m], cu_s[m + int(gs)]))
-        m += int(gs)
-    idx = torch.from_numpy(np.concatenate(order).astype(np.int64)).to(dev["q_pre"].device)
+    from paper_2506_05433_amd.inputs import xours_order
+    tp = prob.total_prefix
+    idx = torch.from_numpy(xours_order(prob)).to(dev["q_pre"].device)
     x = {n: torch.cat([dev[n + "_pre"], dev[n + "_suf"]]).index_select(0, idx) for n in ("q", "k", "v", "do")}
     grp = (dev["cu_prefix"], dev["cu_suffix"], dev["group_sizes"], tp, dev["scale"])
     rows = x["q"].shape[0]

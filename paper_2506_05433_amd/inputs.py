@@ -276,6 +276,19 @@ def make_problem(workload, seed: int = 0, lengths=None, grads: bool = True, peak
     return prob
 
 
+def xours_order(prob: Problem) -> np.ndarray:
+    """Row order of the single-buffer layout of Eq. (2): group after group, the group's prefix rows and then
+    its members' response rows. Entry i is the packed row (prefix rows 0..total_prefix-1, then response rows
+    from total_prefix on) that goes to row i of the single buffer."""
+    cu_p, cu_s, tp = prob.cu_prefix, prob.cu_suffix, prob.total_prefix
+    order, m = [], 0
+    for g, gs in enumerate(prob.group_sizes):
+        order.append(np.arange(cu_p[g], cu_p[g + 1]))
+        order.append(tp + np.arange(cu_s[m], cu_s[m + int(gs)]))
+        m += int(gs)
+    return np.concatenate(order).astype(np.int64) if order else np.zeros(0, np.int64)
+
+
 def repeated_layout(prob: Problem) -> Problem:
     """The repeated-prefix layout of ``prob``: every member gets its own copy of its group's prefix.
 

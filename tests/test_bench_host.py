@@ -166,3 +166,24 @@ def test_prefix_copy_sum_adds_each_groups_copies():
             k += 1
         row += max(gs, 1) * p
     assert row == rows and k == len(run.outs[0]) == 2
+
+
+def test_single_buffer_row_order():
+    """inputs.xours_order: a permutation of the packed rows that puts, group after group, the prefix rows and
+    then the group's members' response rows (Eq. (2)); empty groups and members included."""
+    from paper_2506_05433_amd.inputs import make_problem, xours_order
+    prob = make_problem("single_group", seed=2, lengths=((5, 0, 7, 3), (2, 1, 0, 3), (4, 0, 6, 1, 2, 3)), h_q=4,
+                        h_kv=2, head_dim=64)
+    order = xours_order(prob)
+    tp = prob.total_prefix
+    assert sorted(order.tolist()) == list(range(tp + prob.total_suffix))
+    row, m = 0, 0
+    for g, gs in enumerate(prob.group_sizes):
+        p0, p1 = int(prob.cu_prefix[g]), int(prob.cu_prefix[g + 1])
+        s0, s1 = int(prob.cu_suffix[m]), int(prob.cu_suffix[m + int(gs)])
+        assert order[row:row + p1 - p0].tolist() == list(range(p0, p1))
+        row += p1 - p0
+        assert order[row:row + s1 - s0].tolist() == [tp + r for r in range(s0, s1)]
+        row += s1 - s0
+        m += int(gs)
+    assert row == len(order)

@@ -11,9 +11,8 @@ import os
 import numpy as np
 import pytest
 
-from paper_2506_05433_amd.inputs import make_problem
+from paper_2506_05433_amd.inputs import make_problem, xours_order
 from tests._parity import GRADS, OUTS, to_host
-from tests.test_gpu_xours import xours_order
 
 pytestmark = pytest.mark.gpu
 

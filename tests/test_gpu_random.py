@@ -9,10 +9,9 @@ import numpy as np
 import pytest
 
 from oracle import grouped_oracle, grouped_positions, rope
-from paper_2506_05433_amd.inputs import make_problem
+from paper_2506_05433_amd.inputs import make_problem, xours_order
 from tests._parity import GRADS, OUTS, check, host_view, to_host
 from tests.test_gpu_last import _oracle_last
-from tests.test_gpu_xours import xours_order
 
 pytestmark = pytest.mark.gpu
 

@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 from oracle import grouped_oracle
-from paper_2506_05433_amd.inputs import make_problem
+from paper_2506_05433_amd.inputs import make_problem, xours_order
 from tests._parity import check, host_view, to_host
 from tests.test_gpu_parity import SMALL
 
@@ -22,18 +22,6 @@ def _dev():
     assert torch.cuda.is_available(), "GPU test needs a GPU"
     binding.lib()
     return binding
-
-
-def xours_order(prob):
-    """Packed row (prefix rows 0..tp-1, then response rows tp..) of every row of the single buffer."""
-    cu_p, cu_s = prob.cu_prefix, prob.cu_suffix
-    tp = prob.total_prefix
-    order, m = [], 0
-    for g, gs in enumerate(prob.group_sizes):
-        order.append(np.arange(cu_p[g], cu_p[g + 1]))
-        order.append(tp + np.arange(cu_s[m], cu_s[m + int(gs)]))
-        m += int(gs)
-    return np.concatenate(order).astype(np.int64) if order else np.zeros(0, np.int64)
 
 
 def _run_both(prob):
