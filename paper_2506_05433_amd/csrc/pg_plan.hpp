@@ -72,6 +72,8 @@ struct PlanShared {
 __device__ inline int response_tiles(const int* __restrict__ cu_s, const GroupInfoEx& gi, int b, int split) {
   if (!split) return ceil_div(gi.s1 - gi.s0, b);
   int n = 0;
+  // unrolled so that several members' lengths are loaded at once (one thread walks a group's members)
+#pragma unroll 4
   for (int m = gi.m0; m < gi.m1; ++m) n += ceil_div(cu_s[m + 1] - cu_s[m], b);
   return n;
 }
@@ -196,6 +198,7 @@ __device__ inline int plan_tile(int i, const int* __restrict__ cu_s, int ng, int
     int lo = gi.s0, hi = gi.s1;  // the rows the tile is cut from: the group's, or one member's
     local -= np;
     if (split) {
+#pragma unroll 4
       for (int m = gi.m0; m < gi.m1; ++m) {
         const int t = ceil_div(cu_s[m + 1] - cu_s[m], b);
         if (local < t) {
